@@ -1,0 +1,233 @@
+/*
+ * CPU oracle for the AQLM compressed-weight format and its matrix-vector
+ * product.  TEST INFRASTRUCTURE ONLY: it exists to check the GPU library.
+ * Only the tests, the smoke entry point and the CPU-baseline leg of the
+ * benchmark may load it; the product path never links or calls it, and it
+ * shares no code, header or table with the GPU library.
+ *
+ * What it computes (paper: "Extreme Compression of Large Language Models via
+ * Additive Quantization", Sec. 3 Eq. 2 and Fig. 3):
+ *   - a row i of the weight matrix is split into groups of g consecutive
+ *     inputs; group j is the sum over m = 0..M-1 of codeword b[i][j][m] of
+ *     codebook C_m (Eq. 2), then the whole row is multiplied by the per-output
+ *     scale s_i (Fig. 3, step v; scales per output unit in Sec. 3.3);
+ *   - codebooks and scales are stored in half precision (App. "Estimating
+ *     model size").
+ * Numerical reading fixed here (the paper does not state one):
+ *   - the M codewords are added in fp32 in ascending m, the accumulator
+ *     starting from codeword 0 (so a -0 component survives when M = 1);
+ *   - one fp32 multiply by the scale, then one round-to-nearest-even to fp16,
+ *     fp16 subnormals kept, overflow to +-inf;
+ *   - the matrix-vector product is taken in fp64, ascending input index.
+ * Build with -ffp-contract=off and without -ffast-math so that every fp32
+ * operation is a single IEEE operation in the stated order.
+ *
+ * Layouts (all dense, row-major):
+ *   codes      [d_out][d_in/g][M], m fastest; uint8 when B <= 8, else uint16
+ *   codebooks  [M][2^B][g] fp16 bit patterns
+ *   scales     [d_out] fp16 bit patterns
+ *   W          [d_out][d_in] fp16 bit patterns
+ *   x          [n][d_in] fp16 bit patterns;  y [n][d_out] double
+ *
+ * Return values: 0 ok, 1 null pointer, 2 bad shape, 3 unsupported
+ * (M, B, g), 4 a code outside [0, 2^B).
+ */
+#include <stdint.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_ERR_NULL 1
+#define ORC_ERR_SHAPE 2
+#define ORC_ERR_UNSUPPORTED 3
+#define ORC_ERR_CODE 4
+
+/* ---- IEEE-754 binary16 <-> binary32, written from the format definition ---- */
+
+/* binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits.
+ * Exponent field 0 encodes zero and subnormals (value = frac * 2^-24),
+ * field 31 encodes infinities (frac 0) and NaNs. */
+float oracle_f16_to_f32(uint16_t h) {
+  uint32_t sign = ((uint32_t)h & 0x8000u) << 16;
+  uint32_t exp = ((uint32_t)h >> 10) & 0x1Fu;
+  uint32_t frac = (uint32_t)h & 0x3FFu;
+  uint32_t bits;
+  if (exp == 0) {
+    if (frac == 0) {
+      bits = sign;
+    } else {
+      /* subnormal: normalise frac * 2^-24 into binary32 */
+      int e = -14;
+      while ((frac & 0x400u) == 0) {
+        frac <<= 1;
+        e -= 1;
+      }
+      frac &= 0x3FFu;
+      bits = sign | ((uint32_t)(e + 127) << 23) | (frac << 13);
+    }
+  } else if (exp == 31) {
+    bits = sign | 0x7F800000u | (frac << 13);
+  } else {
+    bits = sign | ((exp - 15u + 127u) << 23) | (frac << 13);
+  }
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return f;
+}
+
+/* Round a binary32 value to the nearest binary16 value, ties to even.
+ * Results below the smallest normal are produced as subnormals; magnitudes
+ * that round above the largest finite value become infinity; NaN stays NaN
+ * (quiet, sign kept). */
+uint16_t oracle_f32_to_f16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, sizeof u);
+  uint32_t sign = (u >> 16) & 0x8000u;
+  uint32_t exp = (u >> 23) & 0xFFu;
+  uint32_t frac = u & 0x7FFFFFu;
+  if (exp == 0xFFu) {
+    if (frac != 0) return (uint16_t)(sign | 0x7E00u | (frac >> 13));
+    return (uint16_t)(sign | 0x7C00u);
+  }
+  int e = (int)exp - 127; /* unbiased exponent (fp32 subnormals give -127) */
+  if (e > 15) return (uint16_t)(sign | 0x7C00u);
+  if (e >= -14) {
+    /* normal binary16 range: keep 10 fraction bits, round on the other 13 */
+    uint32_t h = ((uint32_t)(e + 15) << 10) | (frac >> 13);
+    uint32_t rest = frac & 0x1FFFu;
+    if (rest > 0x1000u || (rest == 0x1000u && (h & 1u))) h += 1u; /* a carry may reach inf */
+    return (uint16_t)(sign | h);
+  }
+  if (e < -25) return (uint16_t)sign; /* below half the smallest subnormal */
+  /* subnormal result: value = sig * 2^(e-23); in units of 2^-24 that is
+   * sig >> shift with shift = -(e + 1) in [14, 24] */
+  uint32_t sig = frac | 0x800000u;
+  int shift = -(e + 1);
+  uint32_t q = sig >> shift;
+  uint32_t rest = sig & ((1u << shift) - 1u);
+  uint32_t half = 1u << (shift - 1);
+  if (rest > half || (rest == half && (q & 1u))) q += 1u; /* may become the smallest normal */
+  return (uint16_t)(sign | q);
+}
+
+void oracle_f32_to_f16_array(const float* in, uint16_t* out, int64_t n) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) out[i] = oracle_f32_to_f16(in[i]);
+}
+
+void oracle_f16_to_f32_array(const uint16_t* in, float* out, int64_t n) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) out[i] = oracle_f16_to_f32(in[i]);
+}
+
+/* ---- dequantization (Eq. 2 with per-output scales, Fig. 3 steps i-v) ---- */
+
+static int check_args(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                      int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g) {
+  if (!codes || !codebooks || !scales) return ORC_ERR_NULL;
+  if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return ORC_ERR_SHAPE;
+  if (M < 1 || M > 64 || B < 1 || B > 16) return ORC_ERR_UNSUPPORTED;
+  return ORC_OK;
+}
+
+static inline uint32_t code_at(const void* codes, int32_t B, int64_t idx) {
+  if (B <= 8) return ((const uint8_t*)codes)[idx];
+  return ((const uint16_t*)codes)[idx];
+}
+
+/* One output row i of the dequantized matrix into w_row[0..d_in). */
+static int dequant_row(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                       int64_t i, int64_t d_in, int32_t M, int32_t B, int32_t g, uint16_t* w_row) {
+  const int64_t groups = d_in / g;
+  const int64_t entries = (int64_t)1 << B;
+  const float s = oracle_f16_to_f32(scales[i]);
+  for (int64_t j = 0; j < groups; ++j) {
+    const int64_t code_base = (i * groups + j) * M;
+    for (int32_t k = 0; k < g; ++k) {
+      float acc = 0.0f;
+      for (int32_t m = 0; m < M; ++m) {
+        const uint32_t c = code_at(codes, B, code_base + m);
+        if ((int64_t)c >= entries) return ORC_ERR_CODE;
+        const float v = oracle_f16_to_f32(codebooks[((int64_t)m * entries + c) * g + k]);
+        if (m == 0)
+          acc = v;
+        else
+          acc = acc + v;
+      }
+      const float t = acc * s;
+      w_row[j * g + k] = oracle_f32_to_f16(t);
+    }
+  }
+  return ORC_OK;
+}
+
+int oracle_dequantize(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                      int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, uint16_t* w_out) {
+  int st = check_args(codes, codebooks, scales, d_out, d_in, M, B, g);
+  if (st != ORC_OK) return st;
+  if (!w_out) return ORC_ERR_NULL;
+  int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+  for (int64_t i = 0; i < d_out; ++i)
+    bad |= dequant_row(codes, codebooks, scales, i, d_in, M, B, g, w_out + i * d_in) != ORC_OK;
+  return bad ? ORC_ERR_CODE : ORC_OK;
+}
+
+/* Dequantize only the listed rows: w_out is [n_rows][d_in]. */
+int oracle_dequantize_rows(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                           int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                           const int64_t* rows, int64_t n_rows, uint16_t* w_out) {
+  int st = check_args(codes, codebooks, scales, d_out, d_in, M, B, g);
+  if (st != ORC_OK) return st;
+  if (!w_out || !rows) return ORC_ERR_NULL;
+  for (int64_t r = 0; r < n_rows; ++r)
+    if (rows[r] < 0 || rows[r] >= d_out) return ORC_ERR_SHAPE;
+  int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+  for (int64_t r = 0; r < n_rows; ++r)
+    bad |= dequant_row(codes, codebooks, scales, rows[r], d_in, M, B, g, w_out + r * d_in) != ORC_OK;
+  return bad ? ORC_ERR_CODE : ORC_OK;
+}
+
+/* ---- dense products on the dequantized fp16 matrix, in fp64 ---- */
+
+/* y[t][i] = sum over c ascending of W[i][c] * x[t][c], every product and sum in
+ * fp64 (the product of two fp16 values is exact in fp64). */
+int oracle_matmul_f16(const uint16_t* w, int64_t d_out, int64_t d_in, const uint16_t* x, int64_t n,
+                      double* y) {
+  if (!w || !x || !y) return ORC_ERR_NULL;
+  if (d_out <= 0 || d_in <= 0 || n <= 0) return ORC_ERR_SHAPE;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < d_out; ++i) {
+    const uint16_t* wr = w + i * d_in;
+    for (int64_t t = 0; t < n; ++t) {
+      const uint16_t* xr = x + t * d_in;
+      double acc = 0.0;
+      for (int64_t c = 0; c < d_in; ++c)
+        acc = acc + (double)oracle_f16_to_f32(wr[c]) * (double)oracle_f16_to_f32(xr[c]);
+      y[t * d_out + i] = acc;
+    }
+  }
+  return ORC_OK;
+}
+
+/* The whole reference path: dequantize (as above) then the fp64 product.
+ * w_scratch must hold d_out * d_in fp16 values; it is left holding W. */
+int oracle_aqlm_matmul(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                       int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, const uint16_t* x,
+                       int64_t n, uint16_t* w_scratch, double* y) {
+  int st = oracle_dequantize(codes, codebooks, scales, d_out, d_in, M, B, g, w_scratch);
+  if (st != ORC_OK) return st;
+  return oracle_matmul_f16(w_scratch, d_out, d_in, x, n, y);
+}
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+/* Threads the parallel loops above use (1 without OpenMP). */
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}

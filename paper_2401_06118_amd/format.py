@@ -1,0 +1,78 @@
+"""Shapes and storage accounting of the AQLM format.
+
+Storage model (paper, App. "Estimating model size"): with fp16 codebooks and
+scales, one layer costs 16*g*M*2^B bits of codebooks, d_out*(d_in/g)*B*M bits
+of codes and 16*d_out bits of scales.  The codes term carries the factor M,
+as the App. equation does (the bullet list above it drops it); the paper's
+worked example and every bitwidth it prints need it.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+
+@dataclass(frozen=True)
+class AqlmShape:
+    d_out: int
+    d_in: int
+    M: int
+    B: int
+    g: int = 8
+
+    @property
+    def groups(self) -> int:
+        return self.d_in // self.g
+
+    @property
+    def code_bytes_per_group(self) -> int:
+        """Bytes the unpacked code tensor spends per group (uint8 or uint16 per code)."""
+        return self.M * (1 if self.B <= 8 else 2)
+
+    def storage_bits(self) -> int:
+        """Bits of the layer under the paper's storage model (B-bit codes, packed)."""
+        return (16 * self.g * self.M * (1 << self.B)
+                + self.d_out * self.groups * self.B * self.M
+                + 16 * self.d_out)
+
+    def bits_per_param(self) -> float:
+        return self.storage_bits() / (self.d_out * self.d_in)
+
+    def codes_bytes(self) -> int:
+        """Bytes of the code tensor as the library stores it (B in {8, 16}: no padding)."""
+        return self.d_out * self.groups * self.code_bytes_per_group
+
+    def codebook_bytes(self) -> int:
+        return self.M * (1 << self.B) * self.g * 2
+
+    def gemv_bytes(self, n: int = 1) -> int:
+        """Algorithmic HBM bytes of one product with n input rows: codes, codebooks,
+        scales, x [n, d_in] and y [n, d_out], each moved once (fp16 activations)."""
+        return (self.codes_bytes() + self.codebook_bytes() + 2 * self.d_out
+                + 2 * n * self.d_in + 2 * n * self.d_out)
+
+    def dequant_bytes(self) -> int:
+        """Algorithmic bytes of dequantization: inputs read once, fp16 W written once."""
+        return self.codes_bytes() + self.codebook_bytes() + 2 * self.d_out + 2 * self.d_out * self.d_in
+
+    def flops(self, n: int = 1) -> int:
+        return 2 * n * self.d_out * self.d_in
+
+
+# Linear layers of one transformer block, (d_out, d_in) per projection, in
+# the order q, k, v, o, gate, up, down.  Llama-2 architecture shapes.
+LLAMA2_BLOCKS = {
+    "7b": (32, [(4096, 4096), (4096, 4096), (4096, 4096), (4096, 4096),
+                (11008, 4096), (11008, 4096), (4096, 11008)]),
+    "13b": (40, [(5120, 5120), (5120, 5120), (5120, 5120), (5120, 5120),
+                 (13824, 5120), (13824, 5120), (5120, 13824)]),
+    "70b": (80, [(8192, 8192), (1024, 8192), (1024, 8192), (8192, 8192),
+                 (28672, 8192), (28672, 8192), (8192, 28672)]),
+}
+
+
+def model_bits_per_param(model: str, M: int, B: int, g: int = 8) -> float:
+    """Average bits per parameter over all linear layers of the transformer blocks."""
+    n_layers, projs = LLAMA2_BLOCKS[model]
+    bits = sum(AqlmShape(o, i, M, B, g).storage_bits() for o, i in projs) * n_layers
+    params = sum(o * i for o, i in projs) * n_layers
+    return bits / params

@@ -1,0 +1,90 @@
+"""Seeded synthetic inputs for the AQLM path.
+
+This module only draws random numbers; it holds none of the method's
+arithmetic.  The same bytes feed the GPU library and the CPU oracle.
+
+Distributions stand in for trained checkpoints (paper, App. "Codebook and
+codes distribution": learned codes are close to uniform, about 15.91 of 16
+bits of entropy, and codebook vectors sit in a ball; scales start at the row
+norm in Sec. 3.3, so the codebooks carry the small magnitudes):
+  codebooks  N(0, 0.02) rounded to fp16, shape [M, 2^B, g]
+  codes      uniform over [0, 2^B), uint8 (B <= 8) or uint16, [d_out, d_in/g, M]
+  scales     U[0.5, 1.5] rounded to fp16, [d_out]
+  x          N(0, 1) rounded to fp16, [n, d_in]
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass
+class Layer:
+    codes: np.ndarray      # [d_out, d_in/g, M] uint8 | uint16
+    codebooks: np.ndarray  # [M, 2^B, g] float16
+    scales: np.ndarray     # [d_out] float16
+    x: np.ndarray          # [n, d_in] float16
+    M: int
+    B: int
+    g: int
+
+    @property
+    def d_out(self) -> int:
+        return self.codes.shape[0]
+
+    @property
+    def d_in(self) -> int:
+        return self.codes.shape[1] * self.g
+
+
+def code_dtype(B: int):
+    return np.uint8 if B <= 8 else np.uint16
+
+
+def layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, n: int = 1,
+          cb_std: float = 0.02) -> Layer:
+    """One random AQLM layer plus an input batch, all from ``seed``."""
+    if d_in % g:
+        raise ValueError("d_in must be a multiple of g")
+    rng = np.random.default_rng(seed)
+    codebooks = rng.normal(0.0, cb_std, size=(M, 1 << B, g)).astype(np.float16)
+    codes = rng.integers(0, 1 << B, size=(d_out, d_in // g, M), dtype=code_dtype(B))
+    scales = rng.uniform(0.5, 1.5, size=d_out).astype(np.float16)
+    x = rng.standard_normal((n, d_in)).astype(np.float16)
+    return Layer(codes, codebooks, scales, x, M, B, g)
+
+
+# fp16 bit patterns that stress rounding: signed zeros, smallest and largest
+# subnormals, smallest normal, values around 1 whose sums land on ties, and
+# the largest finite value (sums of it overflow to infinity after scaling).
+SPECIAL_F16_BITS = np.array(
+    [0x0000, 0x8000, 0x0001, 0x8001, 0x0002, 0x03FF, 0x83FF, 0x0400, 0x8400, 0x0401,
+     0x3C00, 0xBC00, 0x3C01, 0x1000, 0x1400, 0x0C00, 0x3800, 0x7BFF, 0xFBFF, 0x7800,
+     0x3555, 0xB555, 0x2E66, 0x0200, 0x8200],
+    dtype=np.uint16)
+
+
+def special_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, n: int = 1) -> Layer:
+    """A layer whose codebooks and scales mix random finite fp16 bit patterns
+    with ``SPECIAL_F16_BITS`` so that dequantized outputs hit fp16 subnormals,
+    exact ties, signed zeros and overflow."""
+    rng = np.random.default_rng(seed)
+    entries = 1 << B
+    size = M * entries * g
+    raw = rng.integers(0, 1 << 16, size=size, dtype=np.uint32).astype(np.uint16)
+    finite = (raw & 0x7C00) != 0x7C00
+    raw = np.where(finite, raw, raw & 0x83FF)  # turn inf/NaN patterns into subnormals
+    pick = rng.integers(0, SPECIAL_F16_BITS.size, size=size)
+    use_special = rng.random(size) < 0.5
+    cb_bits = np.where(use_special, SPECIAL_F16_BITS[pick], raw).astype(np.uint16)
+    codebooks = cb_bits.reshape(M, entries, g).view(np.float16)
+    sc_choices = np.array([0x3C00, 0x3800, 0x3E00, 0x0400, 0x7BFF, 0x0000, 0x8000, 0xBC00,
+                           0x3C01, 0x1400, 0x0001, 0x5BFF], dtype=np.uint16)
+    sc_bits = np.where(rng.random(d_out) < 0.5, sc_choices[rng.integers(0, sc_choices.size, d_out)],
+                       rng.integers(0x0001, 0x7800, d_out).astype(np.uint16)
+                       | (rng.integers(0, 2, d_out).astype(np.uint16) << 15))
+    scales = sc_bits.astype(np.uint16).view(np.float16)
+    codes = rng.integers(0, entries, size=(d_out, d_in // g, M), dtype=code_dtype(B))
+    x = rng.standard_normal((n, d_in)).astype(np.float16)
+    return Layer(codes, codebooks, scales, x, M, B, g)

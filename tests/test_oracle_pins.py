@@ -1,0 +1,318 @@
+"""Pins of the CPU oracle against things other than itself.
+
+Each test checks the oracle against what the paper or the mathematics fixes:
+brute force from the one-hot form of Eq. 2, closed forms, invariants,
+exhaustive checks of the fp16 rounding against numpy, and the storage
+formula's worked example and printed bitwidths.  None of these touch a GPU.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2401_06118_amd import format as fmt
+from paper_2401_06118_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- fp16 rounding
+
+def test_f16_to_f32_matches_numpy_on_every_pattern():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    mine = oracle.f16_bits_to_f32(bits)
+    ref = bits.view(np.float16).astype(np.float32)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan].view(np.uint32), ref[~nan].view(np.uint32))
+
+
+def test_f32_to_f16_roundtrips_every_finite_f16():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    finite = (bits & 0x7C00) != 0x7C00
+    f = bits[finite].view(np.float16).astype(np.float32)
+    assert np.array_equal(oracle.f32_to_f16_bits(f), bits[finite])
+
+
+def test_f32_to_f16_exhaustive_over_rounding_range():
+    """Every fp32 pattern whose exponent lies where fp16 rounding is not trivial
+    (from below half the smallest subnormal to above the overflow threshold),
+    against numpy's own float32 -> float16 conversion (round to nearest even)."""
+    chunk = 1 << 25
+    for sign in (0, 1):
+        for biased in range(99, 145, 4):  # 4 exponents (2^25 patterns) per chunk
+            start = (sign << 31) | (biased << 23)
+            u = np.arange(start, start + chunk, dtype=np.uint32)
+            f = u.view(np.float32)
+            with np.errstate(over="ignore"):
+                ref = f.astype(np.float16).view(np.uint16)
+            mine = oracle.f32_to_f16_bits(f)
+            bad = np.flatnonzero(ref != mine)
+            assert bad.size == 0, f"first mismatch at {u[bad[0]]:#010x}: {mine[bad[0]]:#06x} vs {ref[bad[0]]:#06x}"
+
+
+def test_f32_to_f16_random_patterns_and_nan():
+    rng = np.random.default_rng(5)
+    u = rng.integers(0, 1 << 32, size=1 << 22, dtype=np.uint64).astype(np.uint32)
+    f = u.view(np.float32)
+    with np.errstate(over="ignore"):
+        ref = f.astype(np.float16)
+    mine = oracle.f32_to_f16_bits(f).view(np.float16)
+    nan = np.isnan(f)
+    assert np.array_equal(np.isnan(mine), nan)
+    assert np.array_equal(mine[~nan].view(np.uint16), ref[~nan].view(np.uint16))
+
+
+@pytest.mark.parametrize("value, expect", [
+    (1.0 + 2.0 ** -11, 0x3C00),                 # tie -> even (down)
+    (1.0 + 3 * 2.0 ** -11, 0x3C02),             # tie -> even (up)
+    (65504.0, 0x7BFF),
+    (65519.99609375, 0x7BFF),                   # just below the overflow threshold
+    (65520.0, 0x7C00),                          # tie at the threshold rounds to inf
+    (-65520.0, 0xFC00),
+    (2.0 ** -24, 0x0001),
+    (2.0 ** -25, 0x0000),                       # tie with zero -> even (zero)
+    (-(2.0 ** -25), 0x8000),
+    (np.nextafter(np.float32(2.0 ** -25), np.float32(1)), 0x0001),
+    (3 * 2.0 ** -25, 0x0002),                   # 1.5 ulp -> even (2)
+    (2.0 ** -14 - 2.0 ** -25, 0x0400),          # largest-subnormal tie rounds up to normal
+    (-0.0, 0x8000),
+    (float("inf"), 0x7C00),
+    (1e-45, 0x0000),                            # fp32 subnormal
+])
+def test_f32_to_f16_named_cases(value, expect):
+    assert int(oracle.f32_to_f16_bits(np.float32(value)).reshape(-1)[0]) == expect
+
+
+# ----------------------------------------------------------- brute force Eq. 2
+
+def brute_force_dequant(codes, codebooks, scales):
+    """Eq. 2 in the paper's own notation: codebook C_m is a g x 2^B matrix whose
+    columns are codewords, b_ijm is a one-hot vector of length 2^B, group (i, j)
+    is sum_m C_m b_ijm and the concatenated row is multiplied by s_i (Fig. 3 v).
+    fp32 sums in ascending m, one fp32 product, numpy's fp16 rounding."""
+    d_out, groups, M = codes.shape
+    _, entries, g = codebooks.shape
+    C = [codebooks[m].astype(np.float32).T for m in range(M)]  # g x 2^B
+    eye = np.eye(entries, dtype=np.float32)
+    rows = []
+    for i in range(d_out):
+        parts = []
+        for j in range(groups):
+            acc = C[0] @ eye[codes[i, j, 0]]
+            for m in range(1, M):
+                acc = (acc + C[m] @ eye[codes[i, j, m]]).astype(np.float32)
+            parts.append(acc)
+        row = np.concatenate(parts).astype(np.float32) * np.float32(scales[i])
+        with np.errstate(over="ignore"):
+            rows.append(row.astype(np.float32).astype(np.float16))
+    return np.stack(rows)
+
+
+@pytest.mark.parametrize("M,B,g", [(1, 2, 8), (2, 2, 8), (3, 3, 4), (4, 4, 2), (2, 4, 8), (1, 4, 1)])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_dequant_matches_one_hot_brute_force(M, B, g, seed):
+    rng = np.random.default_rng(100 * seed + 10 * M + B)
+    d_out, groups = int(rng.integers(1, 9)), int(rng.integers(1, 5))
+    codebooks = rng.standard_normal((M, 1 << B, g)).astype(np.float16)
+    codes = rng.integers(0, 1 << B, size=(d_out, groups, M), dtype=np.uint8)
+    scales = rng.uniform(-2, 2, size=d_out).astype(np.float16)
+    w = oracle.dequantize(codes, codebooks, scales, g).view(np.float16)
+    ref = brute_force_dequant(codes, codebooks, scales)
+    assert w.shape == (d_out, groups * g)
+    assert np.array_equal(w, ref)  # values; +0 and -0 compare equal here
+
+
+def test_dequant_matches_brute_force_on_special_values():
+    lay = synth.special_layer(7, d_out=6, d_in=32, M=3, B=4, g=8)
+    w = oracle.dequantize(lay.codes, lay.codebooks, lay.scales, 8).view(np.float16)
+    ref = brute_force_dequant(lay.codes, lay.codebooks, lay.scales)
+    assert np.array_equal(w, ref)
+    nz = ref != 0
+    assert np.array_equal(w[nz].view(np.uint16), ref[nz].view(np.uint16))
+
+
+def test_exhaustive_code_pairs():
+    """d_out=1, one group, M=2, B=2: all 16 code pairs reconstruct C_0[a] + C_1[b]."""
+    rng = np.random.default_rng(3)
+    codebooks = rng.standard_normal((2, 4, 8)).astype(np.float16)
+    scales = np.array([1.0], dtype=np.float16)
+    for a, b in itertools.product(range(4), range(4)):
+        codes = np.array([[[a, b]]], dtype=np.uint8)
+        w = oracle.dequantize(codes, codebooks, scales, 8).view(np.float16)[0]
+        ref = (codebooks[0, a].astype(np.float32) + codebooks[1, b].astype(np.float32)).astype(np.float16)
+        assert np.array_equal(w, ref), (a, b)
+
+
+def test_summation_order_is_ascending_m():
+    """Codewords 1, 2^-24, -1 in codebooks 0, 1, 2: (1 + 2^-24) rounds to 1 in
+    fp32, so ascending order gives exactly 0; descending order would give 2^-24."""
+    cb = np.zeros((3, 2, 8), dtype=np.float16)
+    cb[0, 1, :] = 1.0
+    cb[1, 1, :] = np.uint16(1).view(np.float16)  # 2^-24, the smallest subnormal
+    cb[2, 1, :] = -1.0
+    codes = np.ones((1, 1, 3), dtype=np.uint8)
+    w = oracle.dequantize(codes, cb, np.ones(1, np.float16), 8)
+    assert np.all(w == 0x0000)
+    codes_rev = codes.copy()
+    cb_rev = cb[::-1].copy()  # now -1, 2^-24, 1: (-1 + 2^-24) + 1 = 2^-24 exactly
+    w_rev = oracle.dequantize(codes_rev, cb_rev, np.ones(1, np.float16), 8)
+    assert np.all(w_rev == 0x0001)
+
+
+def test_negative_zero_codeword_survives_single_codebook():
+    cb = np.zeros((1, 2, 8), dtype=np.float16)
+    cb[0, 0] = -0.0
+    codes = np.zeros((1, 1, 1), dtype=np.uint8)
+    w = oracle.dequantize(codes, cb, np.ones(1, np.float16), 8)
+    assert np.all(w == 0x8000)
+
+
+# --------------------------------------------------------- closed forms, invariants
+
+def test_identity_codebook_reproduces_plain_fp16_matvec():
+    """M=1, B=16: codeword k is the k-th fp16 group of a reference W, codes
+    enumerate the groups, s = 1: the dequantized matrix is W bit for bit and the
+    product equals the exactly rounded fp64 sum up to fp64 rounding."""
+    rng = np.random.default_rng(11)
+    d_out, d_in = 256, 2048
+    w_ref = rng.standard_normal((d_out, d_in)).astype(np.float16)
+    groups = d_in // 8
+    codebooks = w_ref.reshape(1, d_out * groups, 8)
+    assert codebooks.shape[1] == 1 << 16
+    codes = np.arange(d_out * groups, dtype=np.uint32).astype(np.uint16).reshape(d_out, groups, 1)
+    w = oracle.dequantize(codes, codebooks, np.ones(d_out, np.float16), 8)
+    assert np.array_equal(w, w_ref.view(np.uint16))
+    x = rng.standard_normal((1, d_in)).astype(np.float16)
+    y = oracle.matmul_f16(w, x)[0]
+    terms = w_ref.astype(np.float64) * x[0].astype(np.float64)
+    exact = np.array([math.fsum(t) for t in terms])
+    bound = d_in * np.finfo(np.float64).eps * np.abs(terms).sum(axis=1)
+    assert np.all(np.abs(y - exact) <= bound)
+
+
+@pytest.mark.parametrize("M", [1, 2])
+def test_unit_vector_codebook_closed_form(M):
+    """C_0[k] = e_(k mod 8); with M=2 also C_1[k] = 2 e_((k div 8) mod 8).  Then
+    W[i, 8j + t] = s_i (1[t = a mod 8] + 2 * 1[t = (b div 8) mod 8]) and
+    y_i = s_i * sum_j (x[8j + a mod 8] + 2 x[8j + (b div 8) mod 8])."""
+    rng = np.random.default_rng(21 + M)
+    d_out, d_in, B = 64, 96, 8
+    cb = np.zeros((M, 256, 8), dtype=np.float16)
+    k = np.arange(256)
+    cb[0, k, k % 8] = 1.0
+    if M == 2:
+        cb[1, k, (k // 8) % 8] = 2.0
+    codes = rng.integers(0, 256, size=(d_out, d_in // 8, M), dtype=np.uint8)
+    scales = rng.choice(np.array([0.5, 1.0, 1.5, 0.75], np.float16), size=d_out)
+    x = rng.standard_normal((1, d_in)).astype(np.float16)
+    y = oracle.aqlm_matmul(codes, cb, scales, x)[0]
+    xd = x[0].astype(np.float64)
+    j = np.arange(d_in // 8)
+    for i in range(d_out):
+        tot = xd[8 * j + codes[i, :, 0] % 8].copy()
+        if M == 2:
+            tot += 2 * xd[8 * j + (codes[i, :, 1] // 8) % 8]
+        ref = float(scales[i]) * math.fsum(tot)
+        assert abs(y[i] - ref) <= 1e-12 * max(1.0, abs(ref))
+    w = oracle.dequantize(codes, cb, scales).view(np.float16).astype(np.float64)
+    i0, j0 = 3, 5
+    expect = np.zeros(8)
+    expect[codes[i0, j0, 0] % 8] += 1
+    if M == 2:
+        expect[(codes[i0, j0, 1] // 8) % 8] += 2
+    assert np.array_equal(w[i0, 8 * j0:8 * j0 + 8], float(scales[i0]) * expect)
+
+
+def test_zero_scales_give_signed_zeros_and_zero_output():
+    lay = synth.layer(4, 32, 64, 2, 8)
+    zeros = np.zeros(32, dtype=np.float16)
+    w = oracle.dequantize(lay.codes, lay.codebooks, zeros)
+    acc = (lay.codebooks[0][lay.codes[..., 0]].astype(np.float32)
+           + lay.codebooks[1][lay.codes[..., 1]].astype(np.float32)).reshape(32, 64)
+    expect = np.where(np.signbit(acc), 0x8000, 0x0000).astype(np.uint16)
+    assert np.array_equal(w, expect)
+    y = oracle.matmul_f16(w, lay.x)
+    assert np.all(y == 0.0)
+
+
+def test_power_of_two_linearity():
+    lay = synth.layer(8, 48, 128, 2, 8, n=2)
+    y = oracle.aqlm_matmul(lay.codes, lay.codebooks, lay.scales, lay.x)
+    y2 = oracle.aqlm_matmul(lay.codes, lay.codebooks, lay.scales, (lay.x.astype(np.float32) * 2).astype(np.float16))
+    assert np.array_equal(y2, 2 * y)
+    w = oracle.dequantize(lay.codes, lay.codebooks, lay.scales).view(np.float16)
+    w2 = oracle.dequantize(lay.codes, lay.codebooks, (lay.scales.astype(np.float32) * 2).astype(np.float16)).view(np.float16)
+    normal = np.abs(w.astype(np.float32)) >= 2.0 ** -14
+    assert np.array_equal(w2[normal].astype(np.float32), 2 * w[normal].astype(np.float32))
+
+
+def test_codebook_permutation_symmetry():
+    lay = synth.layer(9, 40, 64, 3, 8)
+    rng = np.random.default_rng(9)
+    cb = lay.codebooks.copy()
+    codes = lay.codes.copy()
+    for m in range(3):
+        perm = rng.permutation(256)           # new entry q holds old entry perm[q]
+        inv = np.argsort(perm)                # old code c now lives at inv[c]
+        cb[m] = lay.codebooks[m][perm]
+        codes[..., m] = inv[lay.codes[..., m]].astype(np.uint8)
+    w0 = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+    w1 = oracle.dequantize(codes, cb, lay.scales)
+    assert np.array_equal(w0, w1)
+
+
+def test_two_codebook_swap_symmetry():
+    lay = synth.layer(10, 40, 64, 2, 8)
+    w0 = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+    w1 = oracle.dequantize(np.ascontiguousarray(lay.codes[..., ::-1]),
+                           np.ascontiguousarray(lay.codebooks[::-1]), lay.scales)
+    assert np.array_equal(w0, w1)
+
+
+def test_dequantize_rows_matches_full():
+    lay = synth.layer(12, 100, 64, 4, 8)
+    rows = [0, 99, 17, 17, 50]
+    full = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+    part = oracle.dequantize_rows(lay.codes, lay.codebooks, lay.scales, rows)
+    assert np.array_equal(part, full[rows])
+
+
+def test_matmul_against_exact_sums():
+    rng = np.random.default_rng(13)
+    w = rng.standard_normal((20, 200)).astype(np.float16)
+    x = rng.standard_normal((3, 200)).astype(np.float16)
+    y = oracle.matmul_f16(w, x)
+    for t in range(3):
+        for i in range(20):
+            terms = w[i].astype(np.float64) * x[t].astype(np.float64)
+            exact = math.fsum(terms)
+            assert abs(y[t, i] - exact) <= 200 * np.finfo(np.float64).eps * np.abs(terms).sum()
+
+
+def test_argument_errors():
+    lay = synth.layer(1, 4, 16, 1, 8)
+    with pytest.raises(TypeError):
+        oracle.dequantize(lay.codes.astype(np.uint16), lay.codebooks, lay.scales)
+    with pytest.raises(ValueError):
+        oracle.dequantize(lay.codes, lay.codebooks, lay.scales[:3])
+    cb = np.zeros((1, 4, 8), np.float16)
+    codes = np.full((1, 1, 1), 7, np.uint8)  # code 7 with only 4 entries
+    with pytest.raises(ValueError):
+        oracle.dequantize(codes, cb, np.ones(1, np.float16))
+
+
+# ------------------------------------------------------------- storage formula
+
+def test_size_formula_worked_example_and_printed_bitwidths():
+    with open(os.path.join(GOLDEN, "bitwidths.json")) as f:
+        gold = json.load(f)
+    for e in gold["single_layer"]:
+        bits = fmt.AqlmShape(e["d_out"], e["d_in"], e["M"], e["B"], e["g"]).bits_per_param()
+        assert round(bits, e["decimals"]) == e["bits"], e
+    for e in gold["whole_model"]:
+        assert round(fmt.model_bits_per_param(e["model"], e["M"], e["B"]), 2) == e["bits"], e
