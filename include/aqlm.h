@@ -1,0 +1,98 @@
+/*
+ * aqlm.h - C ABI of the MI355X (gfx950) AQLM inference library.
+ *
+ * AQLM ("Extreme Compression of Large Language Models via Additive
+ * Quantization") stores a weight matrix W [d_out][d_in] as
+ *   - codes: for output row i, input group j (g consecutive inputs) and
+ *     codebook m, an index b[i][j][m] into codebook m (Sec. 3, Eq. 2);
+ *   - codebooks C_m: M tables of 2^B codewords of g fp16 values each;
+ *   - scales s_i: one fp16 scale per output unit (Sec. 3.3, Fig. 3 step v).
+ * Group j of row i reconstructs as s_i * sum_m C_m[b[i][j][m]] (Eq. 2 and
+ * Fig. 3 steps i-v).  The library computes that reconstruction and the
+ * product of it with activations, the operation the paper benchmarks for
+ * token generation (Sec. 4.3, matrix-vector product on one layer).
+ *
+ * Types: fp16 values travel as their IEEE-754 binary16 bit patterns in
+ * uint16_t.  Every pointer is a DEVICE pointer (HIP memory on the current
+ * device) unless stated otherwise.  The caller allocates and owns every
+ * buffer; the library allocates nothing and keeps no state between calls
+ * beyond its loaded kernels, so calls are reentrant and thread-safe.
+ *
+ * Layouts (dense, row-major, contiguous):
+ *   codes      [d_out][d_in/g][M], m fastest.  uint8_t when B = 8,
+ *              uint16_t when B = 16; value = codeword index.
+ *   codebooks  [M][2^B][g] fp16 (one codeword = g contiguous values).
+ *   scales     [d_out] fp16.
+ *   x          [n][d_in] fp16 (n = 1 for the matrix-vector product).
+ *   y          [n][d_out] fp16.
+ *   w_out      [d_out][d_in] fp16.
+ *
+ * Supported formats: g = 8 and either B = 8 with 1 <= M <= 8 (M codebooks of
+ * 256 entries, e.g. the paper's 2x8 and 4x8 schemes) or B = 16 with M = 1 (one
+ * codebook of 65536 entries, the 1x16 scheme).  Sizes: d_out * (d_in / g)
+ * must stay below 2^31 and d_out, n below 2^31.
+ *
+ * Alignment: codes, codebooks, x, y and w_out must be 16-byte aligned and
+ * scales 2-byte aligned.  Shapes whose code row pitch (d_in/g * M * B/8 bytes)
+ * is a multiple of 16 take the vectorized load path; any other shape takes a
+ * slower generic path with the same results.
+ *
+ * Errors: all argument checks run on the host before anything is launched; on
+ * an error nothing is launched and no output is touched.  A HIP launch error
+ * is reported as AQLM_ERR_HIP.  Calls are asynchronous on `stream` (a
+ * hipStream_t; NULL means the default stream): a device-side fault surfaces at
+ * the caller's next synchronisation.  Outputs must not alias inputs.
+ */
+#ifndef AQLM_MI355X_H
+#define AQLM_MI355X_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum aqlm_status {
+  AQLM_OK = 0,
+  AQLM_ERR_NULL = 1,        /* a required pointer is NULL */
+  AQLM_ERR_SHAPE = 2,       /* non-positive or too large size, or d_in % g != 0 */
+  AQLM_ERR_UNSUPPORTED = 3, /* (M, B, g) outside the supported set */
+  AQLM_ERR_ALIGN = 4,       /* a pointer breaks the alignment rule above */
+  AQLM_ERR_HIP = 5          /* the HIP runtime reported an error */
+};
+
+/* Dequantize: w_out[i][j*g + k] = fp16(fp32(sum_m C_m[b[i][j][m]][k]) * s_i)
+ * (Eq. 2, Fig. 3 steps i-v).  The M codewords are added in fp32 in ascending m,
+ * starting from codeword 0, then multiplied by the scale in fp32 and rounded
+ * once to fp16 (nearest, ties to even, subnormals kept, overflow to inf).
+ * The result is bit-exact and deterministic. */
+int aqlm_dequantize(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                    int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                    uint16_t* w_out, void* stream);
+
+/* Matrix-vector product for token generation (Sec. 4.3):
+ * y[i] = fp16(s_i * sum_j sum_m <C_m[b[i][j][m]], x[j*g .. j*g+g)>), fp32
+ * accumulation.  The reconstructed weights are not rounded to fp16 first, and
+ * the summation order differs from a dense product: results agree with
+ * fp16(W) x to fp32 accumulation accuracy, not bit for bit.  Deterministic. */
+int aqlm_gemv(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+              int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+              const uint16_t* x, uint16_t* y, void* stream);
+
+/* Product with n activation rows: y[t][i] = fp16(s_i * sum_c W[i][c] x[t][c])
+ * with W reconstructed as above, fp32 accumulation, any n >= 1.  n = 1 runs
+ * the matrix-vector kernel; larger n runs a matrix-core (MFMA) kernel that
+ * rebuilds each weight fragment once per tile of up to 64 rows of x.
+ * Deterministic. */
+int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                          int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n,
+                          const uint16_t* x, uint16_t* y, void* stream);
+
+/* Static text for a status code (never NULL). */
+const char* aqlm_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AQLM_MI355X_H */

@@ -1,2 +1,99 @@
-"""MI355X-native AQLM inference path: dequantize, GEMV and small-batch GEMM
-on additive-quantized weights, backed by hand-written HIP kernels for gfx950."""
+"""MI355X-native AQLM inference path.
+
+AQLM (Additive Quantization of Language Models) stores a weight matrix as
+codes into M learned codebooks plus one scale per output unit (paper: Sec. 3,
+Eq. 2 and Fig. 3).  This package exposes the three operations of the C ABI in
+``include/aqlm.h`` on torch tensors that live on the GPU:
+
+- :func:`dequantize` - rebuild the fp16 weight matrix, bit-exact;
+- :func:`gemv` - the token-generation matrix-vector product (Sec. 4.3);
+- :func:`gemm_small_batch` - the same product for n activation rows.
+
+Every computation runs in the hand-written HIP kernels of
+``libaqlm_mi355x.so``; this module only marshals arguments.
+
+Tensor formats: ``codes`` uint8 [d_out, d_in/8, M] (B = 8) or uint16/int16
+[d_out, d_in/8, 1] (B = 16); ``codebooks`` fp16 [M, 2^B, 8]; ``scales`` fp16
+[d_out] (a trailing singleton dimension is accepted); activations fp16.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import _lib
+from ._lib import AqlmError, status_string  # noqa: F401
+
+__all__ = ["dequantize", "gemv", "gemm_small_batch", "AqlmError", "status_string", "layer_args"]
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def layer_args(codes: torch.Tensor, codebooks: torch.Tensor, scales: torch.Tensor):
+    """Validate tensor metadata and return (d_out, d_in, M, B, g)."""
+    for name, t in (("codes", codes), ("codebooks", codebooks), ("scales", scales)):
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if codebooks.dtype != torch.float16 or codebooks.dim() != 3:
+        raise ValueError("codebooks must be fp16 [M, 2^B, g]")
+    M, entries, g = codebooks.shape
+    B = int(entries).bit_length() - 1
+    if (1 << B) != entries:
+        raise ValueError("codebook entry count must be a power of two")
+    if codes.dim() != 3 or codes.shape[2] != M:
+        raise ValueError("codes must be [d_out, d_in/g, M]")
+    want = (torch.uint8,) if B <= 8 else (torch.uint16, torch.int16)
+    if codes.dtype not in want:
+        raise ValueError(f"codes for B={B} must be {want[0]}")
+    if scales.dtype != torch.float16 or scales.numel() != codes.shape[0]:
+        raise ValueError("scales must be fp16 with one value per output row")
+    d_out, groups, _ = codes.shape
+    return d_out, groups * g, M, B, g
+
+
+def _check(st: int, what: str):
+    if st != _lib.AQLM_OK:
+        raise AqlmError(st, what)
+
+
+def dequantize(codes, codebooks, scales, *, out=None, stream=None) -> torch.Tensor:
+    """fp16 weight matrix [d_out, d_in]: w[i, 8j+k] = fp16(sum_m C_m[b_ijm][k] * s_i)."""
+    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    if out is None:
+        out = torch.empty((d_out, d_in), dtype=torch.float16, device=codes.device)
+    st = _lib.load().aqlm_dequantize(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in,
+                                     M, B, g, out.data_ptr(), _stream_handle(stream))
+    _check(st, "aqlm_dequantize")
+    return out
+
+
+def gemv(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:
+    """y [d_out] = W x for one fp16 activation vector x [d_in]."""
+    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    if x.dtype != torch.float16 or x.numel() != d_in or not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
+    if out is None:
+        out = torch.empty((d_out,), dtype=torch.float16, device=codes.device)
+    st = _lib.load().aqlm_gemv(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in, M, B, g,
+                               x.data_ptr(), out.data_ptr(), _stream_handle(stream))
+    _check(st, "aqlm_gemv")
+    return out
+
+
+def gemm_small_batch(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:
+    """Y [n, d_out] = X W^T for fp16 activations X [n, d_in]."""
+    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    if x.dtype != torch.float16 or x.dim() != 2 or x.shape[1] != d_in or not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous fp16 GPU tensor [n, d_in]")
+    n = x.shape[0]
+    if out is None:
+        out = torch.empty((n, d_out), dtype=torch.float16, device=codes.device)
+    st = _lib.load().aqlm_gemm_small_batch(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in,
+                                           M, B, g, n, x.data_ptr(), out.data_ptr(), _stream_handle(stream))
+    _check(st, "aqlm_gemm_small_batch")
+    return out

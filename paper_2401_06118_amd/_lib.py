@@ -1,0 +1,62 @@
+"""ctypes binding of ``libaqlm_mi355x.so`` (C ABI in ``include/aqlm.h``).
+
+Argument marshalling only: shapes and dtypes are read from torch tensors,
+device pointers and the current HIP stream are passed through, and every
+step of the computation runs in the library's kernels.  There is no CPU
+fallback: without the built library every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libaqlm_mi355x.so")
+
+AQLM_OK = 0
+STATUS_NAMES = {0: "AQLM_OK", 1: "AQLM_ERR_NULL", 2: "AQLM_ERR_SHAPE", 3: "AQLM_ERR_UNSUPPORTED",
+                4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP"}
+EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemm_small_batch", "aqlm_status_string")
+
+_lock = threading.Lock()
+_lib = None
+
+
+class AqlmError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {STATUS_NAMES.get(status, status)} ({status_string(status)})")
+
+
+def load():
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2401_06118_amd.build` "
+                "(hipcc, gfx950). There is no CPU fallback.")
+        lib = ctypes.CDLL(LIB_PATH)
+        p, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        lib.aqlm_dequantize.argtypes = [p, p, p, i64, i64, i32, i32, i32, p, p]
+        lib.aqlm_dequantize.restype = ctypes.c_int
+        lib.aqlm_gemv.argtypes = [p, p, p, i64, i64, i32, i32, i32, p, p, p]
+        lib.aqlm_gemv.restype = ctypes.c_int
+        lib.aqlm_gemm_small_batch.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p]
+        lib.aqlm_gemm_small_batch.restype = ctypes.c_int
+        lib.aqlm_status_string.argtypes = [ctypes.c_int]
+        lib.aqlm_status_string.restype = ctypes.c_char_p
+        _lib = lib
+        return lib
+
+
+def status_string(status: int) -> str:
+    try:
+        return load().aqlm_status_string(int(status)).decode()
+    except RuntimeError:
+        return STATUS_NAMES.get(status, "unknown")

@@ -1,0 +1,114 @@
+// C ABI of the library (declared in include/aqlm.h): argument validation and
+// dispatch.  Every check runs on the host before any launch; on an error
+// nothing is launched.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdint>
+
+#include "../../include/aqlm.h"
+#include "launch.h"
+
+namespace aqlm {
+
+int num_cus() {
+  static std::atomic<int> cached{0};
+  int v = cached.load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  int dev = 0;
+  hipDeviceProp_t prop;
+  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) return 256;
+  v = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+  cached.store(v, std::memory_order_relaxed);
+  return v;
+}
+
+}  // namespace aqlm
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
+                int32_t M, int32_t B, int32_t g, aqlm::Layer* L) {
+  if (!codes || !codebooks || !scales) return AQLM_ERR_NULL;
+  if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return AQLM_ERR_SHAPE;
+  if (g != 8) return AQLM_ERR_UNSUPPORTED;
+  if (!((B == 8 && M >= 1 && M <= 8) || (B == 16 && M == 1))) return AQLM_ERR_UNSUPPORTED;
+  const int64_t G = d_in / g;
+  if (d_out >= (int64_t(1) << 31) || G >= (int64_t(1) << 31) || d_out * G >= (int64_t(1) << 31))
+    return AQLM_ERR_SHAPE;
+  if (!aligned(codes, 16) || !aligned(codebooks, 16) || !aligned(scales, 2)) return AQLM_ERR_ALIGN;
+  L->codes = codes;
+  L->codebooks = codebooks;
+  L->scales = scales;
+  L->d_out = (int32_t)d_out;
+  L->d_in = (int32_t)d_in;
+  L->G = (int32_t)G;
+  L->M = M;
+  L->B = B;
+  const int64_t pitch = G * M * (B / 8);
+  L->vec_codes = (pitch % 16) == 0;
+  return AQLM_OK;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? AQLM_OK : AQLM_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int aqlm_dequantize(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                    int64_t d_in, int32_t M, int32_t B, int32_t g, uint16_t* w_out, void* stream) {
+  aqlm::Layer L;
+  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  if (!w_out) return AQLM_ERR_NULL;
+  if (!aligned(w_out, 16)) return AQLM_ERR_ALIGN;
+  return status_of(aqlm::launch_dequant(L, w_out, static_cast<hipStream_t>(stream)));
+}
+
+int aqlm_gemv(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
+              int32_t M, int32_t B, int32_t g, const uint16_t* x, uint16_t* y, void* stream) {
+  aqlm::Layer L;
+  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  if (!x || !y) return AQLM_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
+  return status_of(aqlm::launch_gemv(L, x, y, static_cast<hipStream_t>(stream)));
+}
+
+int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                          int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
+                          void* stream) {
+  aqlm::Layer L;
+  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  if (!x || !y) return AQLM_ERR_NULL;
+  if (n <= 0 || n >= (int64_t(1) << 31) || n * d_in >= (int64_t(1) << 40)) return AQLM_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n == 1) return status_of(aqlm::launch_gemv(L, x, y, s));
+  if (aqlm::mfma_supported(L)) return status_of(aqlm::launch_gemm_mfma(L, (int32_t)n, x, y, s));
+  // Formats the matrix-core kernel does not tile (M = 3, 5, 6, 7): one
+  // matrix-vector launch per activation row.
+  for (int64_t t = 0; t < n; ++t) {
+    const hipError_t e = aqlm::launch_gemv(L, x + t * d_in, y + t * d_out, s);
+    if (e != hipSuccess) return AQLM_ERR_HIP;
+  }
+  return AQLM_OK;
+}
+
+const char* aqlm_status_string(int status) {
+  switch (status) {
+    case AQLM_OK: return "ok";
+    case AQLM_ERR_NULL: return "null pointer argument";
+    case AQLM_ERR_SHAPE: return "invalid shape";
+    case AQLM_ERR_UNSUPPORTED: return "unsupported (M, B, g)";
+    case AQLM_ERR_ALIGN: return "misaligned pointer";
+    case AQLM_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

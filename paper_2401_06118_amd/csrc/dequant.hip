@@ -1,0 +1,117 @@
+// Dequantization of AQLM weights to fp16 (Eq. 2 with per-output scales,
+// Fig. 3 steps i-v), bit-exact by construction:
+//   acc = C_0[b_0][k]; acc = acc + C_m[b_m][k] for m = 1..M-1   (fp32, ascending m)
+//   w   = fp16_rne(acc * s_i)                                     (one fp32 product)
+// Each thread writes one group of 8 weights (16 bytes); consecutive threads
+// write consecutive groups, so both the code reads and the fp16 writes are
+// fully coalesced.  The kernel is bound by the 16-byte-per-group write
+// stream.  For B = 8 the M codebooks (4 KiB each) sit in LDS; for B = 16 the
+// 1 MiB codebook is read through L2.
+#include "common.h"
+#include "launch.h"
+
+namespace aqlm {
+
+template <int M, int B>
+__device__ __forceinline__ void load_group_codes(const void* __restrict__ codes, uint32_t q, uint32_t (&c)[M]) {
+  if constexpr (B == 16) {
+    c[0] = static_cast<const uint16_t*>(codes)[q];
+  } else {
+    const uint8_t* p = static_cast<const uint8_t*>(codes) + (size_t)q * M;
+    if constexpr (M == 2) {
+      const uint32_t v = *reinterpret_cast<const uint16_t*>(p);
+      c[0] = v & 0xFF;
+      c[1] = v >> 8;
+    } else if constexpr (M == 4) {
+      const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) c[m] = byte_of(v, m);
+    } else if constexpr (M == 8) {
+      const uint2 v = *reinterpret_cast<const uint2*>(p);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        c[m] = byte_of(v.x, m);
+        c[m + 4] = byte_of(v.y, m);
+      }
+    } else {
+#pragma unroll
+      for (int m = 0; m < M; ++m) c[m] = p[m];
+    }
+  }
+}
+
+__device__ __forceinline__ void unpack8(const uint4& v, float (&f)[8]) {
+  f[0] = h2f(v.x & 0xFFFF); f[1] = h2f(v.x >> 16);
+  f[2] = h2f(v.y & 0xFFFF); f[3] = h2f(v.y >> 16);
+  f[4] = h2f(v.z & 0xFFFF); f[5] = h2f(v.z >> 16);
+  f[6] = h2f(v.w & 0xFFFF); f[7] = h2f(v.w >> 16);
+}
+
+template <int M, int B>
+__global__ __launch_bounds__(256) void k_dequant(const void* __restrict__ codes, const uint4* __restrict__ cb,
+                                                 const uint16_t* __restrict__ scales, uint32_t total_groups,
+                                                 uint32_t G, uint4* __restrict__ w) {
+#pragma clang fp contract(off)
+  constexpr int kLdsEntries = (B == 8) ? M * 256 : 1;
+  __shared__ uint4 cb_lds[kLdsEntries];
+  if constexpr (B == 8) {
+    for (int e = threadIdx.x; e < M * 256; e += 256) cb_lds[e] = cb[e];
+    __syncthreads();
+  }
+  const uint32_t stride = gridDim.x * 256u;
+  for (uint32_t q = blockIdx.x * 256u + threadIdx.x; q < total_groups; q += stride) {
+    const uint32_t row = q / G;
+    const float s = h2f(scales[row]);
+    uint32_t c[M];
+    load_group_codes<M, B>(codes, q, c);
+    float acc[8];
+    unpack8((B == 8) ? cb_lds[c[0]] : cb[c[0]], acc);
+#pragma unroll
+    for (int m = 1; m < M; ++m) {
+      float v[8];
+      unpack8(cb_lds[m * 256 + c[m]], v);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] = acc[k] + v[k];
+    }
+    uint32_t h[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      // The empty asm keeps the fp32 product as its own rounding step: without
+      // it the backend folds product and conversion into one v_fma_mixlo_f16,
+      // which rounds once (and turns a -0 product into +0).
+      float t = acc[k] * s;
+      asm volatile("" : "+v"(t));
+      h[k] = f2h(t);
+    }
+    w[q] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+  }
+}
+
+template <int M, int B>
+static hipError_t run_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
+  const uint32_t total = (uint32_t)L.d_out * (uint32_t)L.G;
+  uint32_t blocks = (total + 255u) / 256u;
+  const uint32_t cap = (uint32_t)num_cus() * 8u;
+  if (blocks > cap) blocks = cap;
+  hipLaunchKernelGGL((k_dequant<M, B>), dim3(blocks), dim3(256), 0, s, L.codes,
+                     reinterpret_cast<const uint4*>(L.codebooks), L.scales, total, (uint32_t)L.G,
+                     reinterpret_cast<uint4*>(w));
+  return hipGetLastError();
+}
+
+hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
+  if (L.B == 16) return run_dequant<1, 16>(L, w, s);
+  switch (L.M) {
+    case 1: return run_dequant<1, 8>(L, w, s);
+    case 2: return run_dequant<2, 8>(L, w, s);
+    case 3: return run_dequant<3, 8>(L, w, s);
+    case 4: return run_dequant<4, 8>(L, w, s);
+    case 5: return run_dequant<5, 8>(L, w, s);
+    case 6: return run_dequant<6, 8>(L, w, s);
+    case 7: return run_dequant<7, 8>(L, w, s);
+    case 8: return run_dequant<8, 8>(L, w, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace aqlm

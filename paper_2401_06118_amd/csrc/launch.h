@@ -1,0 +1,30 @@
+// Internal launchers (C++ linkage) behind the C ABI in include/aqlm.h.
+// Arguments are already validated by the caller; every function returns a
+// hipError_t from the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace aqlm {
+
+struct Layer {
+  const void* codes;          // [d_out][G][M] uint8 (B = 8) or uint16 (B = 16)
+  const uint16_t* codebooks;  // [M][2^B][8] fp16
+  const uint16_t* scales;     // [d_out] fp16
+  int32_t d_out;
+  int32_t d_in;
+  int32_t G;  // d_in / 8
+  int32_t M;
+  int32_t B;
+  bool vec_codes;  // codes base 16-byte aligned and row pitch a multiple of 16 bytes
+};
+
+hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s);
+hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s);
+hipError_t launch_gemm_mfma(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
+bool mfma_supported(const Layer& L);
+
+int num_cus();
+
+}  // namespace aqlm

@@ -1,0 +1,114 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+include/aqlm.h declares, and rejects bad arguments before touching the GPU
+(argument validation dereferences nothing, so fake pointers suffice)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2401_06118_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "aqlm.h")
+
+OK, NULL, SHAPE, UNSUP, ALIGN = 0, 1, 2, 3, 4
+P = 0x10000  # a 64 KiB-aligned fake device address; never dereferenced on error paths
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(aqlm_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.skip("library not built (run python -m paper_2401_06118_amd.build)")
+    return _lib.load()
+
+
+def test_header_declares_the_three_operations():
+    assert set(declared_functions()) >= {"aqlm_dequantize", "aqlm_gemv", "aqlm_gemm_small_batch",
+                                         "aqlm_status_string"}
+
+
+def test_library_exports_every_declared_function(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert set(_lib.EXPORTS) <= set(declared_functions())
+
+
+def test_status_strings(lib):
+    for st in range(6):
+        assert lib.aqlm_status_string(st)
+    assert lib.aqlm_status_string(99) == b"unknown status"
+
+
+def gemv(lib, codes=P, cb=P, sc=P, d_out=64, d_in=64, M=2, B=8, g=8, x=P, y=P):
+    return lib.aqlm_gemv(codes, cb, sc, d_out, d_in, M, B, g, x, y, None)
+
+
+def gemm(lib, n=4, codes=P, cb=P, sc=P, d_out=64, d_in=64, M=2, B=8, g=8, x=P, y=P):
+    return lib.aqlm_gemm_small_batch(codes, cb, sc, d_out, d_in, M, B, g, n, x, y, None)
+
+
+def deq(lib, codes=P, cb=P, sc=P, d_out=64, d_in=64, M=2, B=8, g=8, w=P):
+    return lib.aqlm_dequantize(codes, cb, sc, d_out, d_in, M, B, g, w, None)
+
+
+@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+def test_null_pointers(lib, fn):
+    for kw in ("codes", "cb", "sc"):
+        assert fn(lib, **{kw: None}) == NULL
+    if fn is deq:
+        assert fn(lib, w=None) == NULL
+    else:
+        assert fn(lib, x=None) == NULL
+        assert fn(lib, y=None) == NULL
+
+
+@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+def test_shapes(lib, fn):
+    assert fn(lib, d_out=0) == SHAPE
+    assert fn(lib, d_out=-3) == SHAPE
+    assert fn(lib, d_in=0) == SHAPE
+    assert fn(lib, d_in=12) == SHAPE          # not a multiple of g
+    assert fn(lib, d_out=1 << 20, d_in=1 << 14) == SHAPE  # d_out * d_in/g >= 2^31
+
+
+def test_gemm_batch_size(lib):
+    assert gemm(lib, n=0) == SHAPE
+    assert gemm(lib, n=-1) == SHAPE
+
+
+@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+def test_unsupported_formats(lib, fn):
+    assert fn(lib, g=4, d_in=64) == UNSUP
+    assert fn(lib, M=0) == UNSUP
+    assert fn(lib, M=9) == UNSUP
+    assert fn(lib, M=2, B=16) == UNSUP
+    assert fn(lib, M=1, B=12) == UNSUP
+    assert fn(lib, M=1, B=4) == UNSUP
+
+
+@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+def test_alignment(lib, fn):
+    assert fn(lib, codes=P + 1) == ALIGN
+    assert fn(lib, cb=P + 8) == ALIGN
+    assert fn(lib, sc=P + 1) == ALIGN
+    if fn is deq:
+        assert fn(lib, w=P + 2) == ALIGN
+    else:
+        assert fn(lib, x=P + 2) == ALIGN
+        assert fn(lib, y=P + 4) == ALIGN
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    import paper_2401_06118_amd as aq
+    codes = torch.zeros((4, 2, 2), dtype=torch.uint8)
+    cb = torch.zeros((2, 256, 8), dtype=torch.float16)
+    sc = torch.ones(4, dtype=torch.float16)
+    with pytest.raises(ValueError):
+        aq.dequantize(codes, cb, sc)
