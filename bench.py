@@ -1,0 +1,406 @@
+#!/usr/bin/env python3
+"""Benchmark of the AQLM token-generation product on one MI355X.
+
+Default workload (one "step"): the linear layers of one Llama-2-7B decode step
+at batch 1 - 32 blocks x {q, k, v, o: 4096x4096; gate, up: 11008x4096; down:
+4096x11008} = 224 AQLM 2x8 (g = 8) matrix-vector products, each layer with
+its own random codes, codebooks, scales and input vector, all resident in HBM,
+launched back to back on one stream.  ``value`` is the step's algorithmic HBM
+bytes (codes + codebooks + scales + x + y of every layer) divided by the
+measured step time; tokens/s-equivalent is 1 / step time (linear layers only:
+attention, norms, embeddings and the LM head are not part of the step).
+
+Also reported on the same JSON line:
+  roofline      the dominant kernel (the matrix-vector kernel) against 8 TB/s,
+                with its average duration from HIP events around each launch;
+  cpu_baseline  the CPU oracle (dequantize + fp64 product) timed on the host
+                cores on a sample of the step's layers, scaled to the step;
+  secondary     the same step in the 1x16 scheme, single layers rotated over
+                >= 1 GiB of replicas (so HBM, not the 256 MB MALL, is measured),
+                the small-batch / prefill products and dequantization.
+
+Only one GPU is supported: --gpus N with N > 1 exits with a message.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, vendor peak
+MFMA_F16_PEAK_TFS = 2500.0  # MI355X dense fp16 matrix peak
+
+WORKLOADS = {
+    # name: (model shapes key, M, B)
+    "llama2-7b-2x8": ("7b", 2, 8),
+    "llama2-7b-1x16": ("7b", 1, 16),
+    "llama2-70b-2x8": ("70b", 2, 8),
+}
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama2-7b-2x8", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
+    return ap.parse_args()
+
+
+class DeviceLayer:
+    def __init__(self, seed, d_out, d_in, M, B, n=1, x=None):
+        from paper_2401_06118_amd import format as fmt
+        from paper_2401_06118_amd import synth
+        self.shape = fmt.AqlmShape(d_out, d_in, M, B)
+        self.codes, self.codebooks, self.scales, xg = synth.device_layer(seed, d_out, d_in, M, B, n=n)
+        self.x = xg if x is None else x
+        import torch
+        self.y = torch.empty((n, d_out), dtype=torch.float16, device="cuda")
+        self.n = n
+
+    def problem(self):
+        return (self.codes, self.codebooks, self.scales, self.x[0], self.y[0])
+
+    def gemv(self, aq):
+        aq.gemv(self.codes, self.codebooks, self.scales, self.x[0], out=self.y[0])
+
+    def gemm(self, aq):
+        aq.gemm_small_batch(self.codes, self.codebooks, self.scales, self.x, out=self.y)
+
+
+def decode_step_layers(model: str, M: int, B: int, seed0: int):
+    """Per block, in order: q, k, v, o, gate, up, down.  q/k/v read one shared
+    input vector and gate/up another, as in the model."""
+    import torch
+
+    from paper_2401_06118_amd import format as fmt
+    n_blocks, projs = fmt.LLAMA2_BLOCKS[model]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(seed0 + 7)
+    layers = []
+    for b in range(n_blocks):
+        x_attn = torch.randn((1, projs[0][1]), device="cuda", generator=gen).half()
+        x_mlp = torch.randn((1, projs[4][1]), device="cuda", generator=gen).half()
+        shared = {0: x_attn, 1: x_attn, 2: x_attn, 4: x_mlp, 5: x_mlp}
+        for p, (d_out, d_in) in enumerate(projs):
+            layers.append(DeviceLayer(seed0 + 16 * b + p, d_out, d_in, M, B, x=shared.get(p)))
+    return layers
+
+
+def launches_by_dependency(layers, aq):
+    """One launch per dependency level of a block: grouped (q, k, v), o,
+    grouped (gate, up), down."""
+    out = []
+    for b in range(0, len(layers), 7):
+        q, k, v, o, gate, up, down = layers[b:b + 7]
+        out.append(lambda q=q, k=k, v=v: aq.gemv_grouped([q.problem(), k.problem(), v.problem()]))
+        out.append(lambda o=o: o.gemv(aq))
+        out.append(lambda gate=gate, up=up: aq.gemv_grouped([gate.problem(), up.problem()]))
+        out.append(lambda down=down: down.gemv(aq))
+    return out
+
+
+def graph_of(launches):
+    """Capture the launch list into one HIP graph (torch.cuda.CUDAGraph)."""
+    import torch
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for fn in launches:  # warm-up outside capture (sets kernel attributes once)
+            fn()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for fn in launches:
+            fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def time_steps(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps  # ms
+
+
+def per_launch_ms(launches, reps):
+    """Average duration of each launch, from a HIP event pair recorded around it
+    on the launching (torch current) stream, over `reps` passes.  Each pass
+    starts behind a spin kernel long enough for the host to queue every event
+    and launch first, so the pairs time the GPU, not the host's enqueue rate."""
+    import torch
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
+          for _ in range(reps)]
+    torch.cuda.synchronize()
+    for r in range(reps):
+        torch.cuda._sleep(int(2.4e9 * (0.005 + 60e-6 * len(launches))))
+        for (a, b), fn in zip(ev[r], launches):
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+    return [sum(ev[r][i][0].elapsed_time(ev[r][i][1]) for r in range(reps)) / reps for i in range(len(launches))]
+
+
+def source_digest(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2401_06118_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel_key: str, digest: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None if there is none for this kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        parts = line.split()
+        if len(parts) >= 3 and parts[0] == kernel_key and parts[1] == digest:
+            return float(parts[2])
+    return None
+
+
+def cpu_baseline(layers, budget_s):
+    """Oracle (dequantize + fp64 product) on the host cores, one layer of each
+    distinct shape, repeated until the budget is spent; scaled to the step."""
+    import numpy as np
+
+    import oracle
+    shapes = {}
+    for L in layers:
+        shapes.setdefault((L.shape.d_out, L.shape.d_in), []).append(L)
+    per_shape = {}
+    host = {}
+    for key, ls in shapes.items():
+        L = ls[0]
+        codes = L.codes.cpu().numpy()
+        if L.shape.B == 16:
+            codes = codes.view(np.uint16)
+        host[key] = (codes, L.codebooks.cpu().numpy(), L.scales.cpu().numpy(), L.x.cpu().numpy())
+        per_shape[key] = []
+    t_end = time.perf_counter() + budget_s
+    rounds = 0
+    while True:
+        for key, (codes, cb, sc, x) in host.items():
+            t0 = time.perf_counter()
+            oracle.aqlm_matmul(codes, cb, sc, x)
+            per_shape[key].append(time.perf_counter() - t0)
+        rounds += 1
+        if time.perf_counter() > t_end or rounds >= 50:
+            break
+    step_s = sum(len(shapes[k]) * float(np.median(v)) for k, v in per_shape.items())
+    step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
+    return {
+        "value": step_bytes / step_s / 1e9,
+        "unit": "GB/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"one layer of each of the {len(shapes)} distinct shapes, dequantize + fp64 product, "
+                   f"median of {rounds} runs each, step time = sum over shapes of count x median "
+                   f"({step_s:.3f} s per step, {1.0 / step_s:.4f} tok/s-eq)"),
+    }
+
+
+def single_layer_rows(aq, torch):
+    """Single layers rotated over >= 1 GiB of replicas so each call reads HBM."""
+    rows = []
+    for name, (d_out, d_in, M, B) in {
+        "4096x4096 2x8": (4096, 4096, 2, 8),
+        "4096x4096 1x16": (4096, 4096, 1, 16),
+        "11008x4096 1x16": (11008, 4096, 1, 16),
+        "4096x11008 1x16": (4096, 11008, 1, 16),
+        "28672x8192 2x8": (28672, 8192, 2, 8),
+    }.items():
+        from paper_2401_06118_amd import format as fmt
+        shp = fmt.AqlmShape(d_out, d_in, M, B)
+        reps = max(2, min(256, (1 << 30) // shp.codes_bytes() + 1))
+        layers = [DeviceLayer(900000 + i, d_out, d_in, M, B) for i in range(reps)]
+        calls = [lambda L=L: L.gemv(aq) for L in layers]
+        g = graph_of(calls)
+        ms = time_steps(g.replay, steps=3, warmup=1) / reps
+        kern = per_launch_ms(calls[: min(reps, 64)], reps=2)
+        kern_ms = sum(kern) / len(kern)
+        del g
+        b = shp.gemv_bytes(1)
+        rows.append({"layer": name, "bytes": b, "us_per_call": ms * 1e3, "kernel_us": kern_ms * 1e3,
+                     "GBs_wall": b / (ms * 1e6), "GBs_kernel": b / (kern_ms * 1e6),
+                     "frac_kernel": b / (kern_ms * 1e6) / HBM_PEAK_GBS, "replicas": reps})
+        del layers
+        torch.cuda.empty_cache()
+    return rows
+
+
+def batch_rows(aq, torch):
+    """11008x4096 1x16 and 4x8 with n activation rows (the small-batch and
+    prefill path), plus dequantization of the same layers."""
+    rows = []
+    for M, B in ((1, 16), (4, 8)):
+        for n in (1, 4, 16, 256, 2048):
+            from paper_2401_06118_amd import format as fmt
+            shp = fmt.AqlmShape(11008, 4096, M, B)
+            reps = 1 if n >= 256 else max(2, (1 << 30) // shp.codes_bytes() + 1)
+            layers = [DeviceLayer(800000 + 7 * i + n, 11008, 4096, M, B, n=n) for i in range(reps)]
+            g = graph_of([lambda L=L: L.gemm(aq) for L in layers])
+            ms = time_steps(g.replay, steps=max(3, 8 // reps), warmup=1) / reps
+            del g
+            b = shp.gemv_bytes(n)
+            rows.append({"layer": f"11008x4096 {M}x{B // 8 * 8 if B == 8 else 16}", "n": n, "us": ms * 1e3,
+                         "GBs": b / (ms * 1e6), "TFLOPs": shp.flops(n) / (ms * 1e9),
+                         "mfma_frac": shp.flops(n) / (ms * 1e9) / MFMA_F16_PEAK_TFS})
+            del layers
+            torch.cuda.empty_cache()
+        L = DeviceLayer(700000 + M, 11008, 4096, M, B)
+        w = torch.empty((11008, 4096), dtype=torch.float16, device="cuda")
+        ms = time_steps(lambda: aq.dequantize(L.codes, L.codebooks, L.scales, out=w), steps=10, warmup=3)
+        rows.append({"layer": f"11008x4096 M={M} B={B}", "op": "dequantize", "us": ms * 1e3,
+                     "GBs": L.shape.dequant_bytes() / (ms * 1e6)})
+        del w, L
+        torch.cuda.empty_cache()
+    return rows
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(no multi-GPU path exists).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2401_06118_amd as aq
+    from paper_2401_06118_amd import _lib
+
+    _lib.load()  # fail loudly if the HIP library is missing
+    model, M, B = WORKLOADS[args.workload]
+    layers = decode_step_layers(model, M, B, seed0=1000 * (1 if M == 2 else 2))
+    step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
+    launches = launches_by_dependency(layers, aq)
+    log(f"{args.workload}: {len(layers)} layers in {len(launches)} launches, {step_bytes / 1e9:.3f} GB per step")
+    graph = graph_of(launches)
+    ms = time_steps(graph.replay, args.steps, args.warmup)
+    log(f"step {ms:.4f} ms (graph replay)")
+
+    # Dominant kernel: every launch of the step is the matrix-vector kernel
+    # (grouped or single); its average duration from an event pair per launch.
+    kern = per_launch_ms(launches, reps=max(2, min(args.steps, 5)))
+    kern_total_ms = sum(kern)
+    avg_launch_ms = kern_total_ms / len(launches)
+    bytes_per_launch = step_bytes / len(launches)
+    achieved = bytes_per_launch / (avg_launch_ms * 1e6)
+    digest = source_digest("gemv_mfma.hip", "common.h")
+    traffic = measured_traffic(f"gemv_{model}_{M}x{B}", digest)
+
+    result = {
+        "metric": "achieved HBM GB/s & roofline % for AQLM GEMV (batch 1); decode tokens/s-equivalent",
+        "value": step_bytes / (ms * 1e6),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16 (fp32 accumulate)",
+        "data": "synthetic: uniform codes, N(0,0.02) fp16 codebooks, U[0.5,1.5] fp16 scales, N(0,1) fp16 x",
+        "config": {
+            "workload": f"Llama-2-{model.upper()} decode step, linear layers only, AQLM {M}x{B if B == 16 else 8} "
+                        f"g8, batch 1: {len(layers)} GEMVs in {len(launches)} launches (per block: grouped "
+                        f"q/k/v, o, grouped gate/up, down), replayed as one HIP graph",
+            "layers": len(layers),
+            "launches": len(launches),
+            "bytes_per_step": step_bytes,
+            "parallelism": "single GPU",
+        },
+        "tokens_per_s_equivalent": 1000.0 / ms,
+        "roofline_frac_step": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
+        "kernel_only": {"sum_kernel_ms": kern_total_ms, "GBs": step_bytes / (kern_total_ms * 1e6),
+                        "tok_s_eq": 1000.0 / kern_total_ms},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": f"k_gemv_mfma<M={M},B={B}>",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "bytes_per_launch": bytes_per_launch,
+            "avg_launch_us": avg_launch_ms * 1e3,
+        },
+    }
+
+    if not args.no_secondary:
+        sec = {}
+        # the same step without grouping: 224 single launches, one graph
+        g1 = graph_of([lambda L=L: L.gemv(aq) for L in layers])
+        ms1 = time_steps(g1.replay, args.steps, 2)
+        sec["ungrouped_224_launches"] = {"ms_per_step": ms1, "GBs": step_bytes / (ms1 * 1e6),
+                                         "tok_s_eq": 1000.0 / ms1}
+        # upper bound without the block's dependencies: 8 independent GEMVs per launch
+        fused = [lambda c=layers[i:i + 8]: aq.gemv_grouped([L.problem() for L in c])
+                 for i in range(0, len(layers), 8)]
+        g8 = graph_of(fused)
+        ms8 = time_steps(g8.replay, args.steps, 2)
+        sec["independent_8_per_launch"] = {"launches": len(fused), "ms_per_step": ms8,
+                                           "GBs": step_bytes / (ms8 * 1e6), "tok_s_eq": 1000.0 / ms8}
+        del g1, g8
+        log(f"ungrouped {ms1:.4f} ms, 8-per-launch {ms8:.4f} ms")
+        other = "llama2-7b-1x16" if args.workload != "llama2-7b-1x16" else "llama2-7b-2x8"
+        om, oM, oB = WORKLOADS[other]
+        del layers, launches, graph
+        torch.cuda.empty_cache()
+        olayers = decode_step_layers(om, oM, oB, seed0=5000)
+        ob = sum(L.shape.gemv_bytes(1) for L in olayers)
+        olaunch = launches_by_dependency(olayers, aq)
+        og = graph_of(olaunch)
+        oms = time_steps(og.replay, max(5, args.steps // 2), 2)
+        okern = per_launch_ms(olaunch, reps=2)
+        sec[other] = {"ms_per_step": oms, "GBs": ob / (oms * 1e6), "frac": ob / (oms * 1e6) / HBM_PEAK_GBS,
+                      "tok_s_eq": 1000.0 / oms, "kernel_sum_ms": sum(okern),
+                      "GBs_kernel": ob / (sum(okern) * 1e6)}
+        del olayers, olaunch, og
+        torch.cuda.empty_cache()
+        log(f"{other}: {oms:.4f} ms per step")
+        sec["single_layers"] = single_layer_rows(aq, torch)
+        log("single layers done")
+        sec["batch"] = batch_rows(aq, torch)
+        log("batch / dequantize done")
+        result["secondary"] = sec
+        layers = None
+    if not args.no_cpu_baseline:
+        if layers is None:
+            layers = decode_step_layers(model, M, B, seed0=1000 * (1 if M == 2 else 2))
+        log("cpu baseline (oracle) ...")
+        result["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

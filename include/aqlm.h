@@ -79,6 +79,33 @@ int aqlm_gemv(const void* codes, const uint16_t* codebooks, const uint16_t* scal
               int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
               const uint16_t* x, uint16_t* y, void* stream);
 
+/* One problem of a grouped matrix-vector launch (all pointers device memory,
+ * same layouts and rules as aqlm_gemv). */
+typedef struct aqlm_gemv_problem {
+  const void* codes;
+  const uint16_t* codebooks;
+  const uint16_t* scales;
+  const uint16_t* x; /* [d_in] */
+  uint16_t* y;       /* [d_out] */
+  int64_t d_out;
+  int64_t d_in;
+} aqlm_gemv_problem;
+
+#define AQLM_MAX_GROUPED 8
+
+/* `count` (1..AQLM_MAX_GROUPED) independent matrix-vector products that share
+ * (M, B, g), computed as aqlm_gemv would compute each, in one launch - for
+ * layers that read the same activation, such as the q, k and v projections or
+ * the gate and up projections of a transformer block (the paper's speed
+ * measurement is per layer, Sec. 4.3; grouping only removes launch overhead).
+ * `problems` is a HOST array read during the call.  Every problem is
+ * validated before anything is launched; the first error is returned.
+ * Outputs must not alias any input of any problem.  Deterministic; results
+ * may differ from separate aqlm_gemv calls in the last bits because the rows
+ * are split over workgroups differently. */
+int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                      void* stream);
+
 /* Product with n activation rows: y[t][i] = fp16(s_i * sum_c W[i][c] x[t][c])
  * with W reconstructed as above, fp32 accumulation, any n >= 1.  n = 1 runs
  * the matrix-vector kernel; larger n runs a matrix-core (MFMA) kernel that

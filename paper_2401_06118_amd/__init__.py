@@ -7,6 +7,7 @@ Eq. 2 and Fig. 3).  This package exposes the three operations of the C ABI in
 
 - :func:`dequantize` - rebuild the fp16 weight matrix, bit-exact;
 - :func:`gemv` - the token-generation matrix-vector product (Sec. 4.3);
+- :func:`gemv_grouped` - several independent matrix-vector products in one launch;
 - :func:`gemm_small_batch` - the same product for n activation rows.
 
 Every computation runs in the hand-written HIP kernels of
@@ -23,7 +24,7 @@ import torch
 from . import _lib
 from ._lib import AqlmError, status_string  # noqa: F401
 
-__all__ = ["dequantize", "gemv", "gemm_small_batch", "AqlmError", "status_string", "layer_args"]
+__all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "AqlmError", "status_string", "layer_args"]
 
 
 def _stream_handle(stream) -> int:
@@ -83,6 +84,30 @@ def gemv(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:
                                x.data_ptr(), out.data_ptr(), _stream_handle(stream))
     _check(st, "aqlm_gemv")
     return out
+
+
+def gemv_grouped(problems, *, stream=None):
+    """Independent products [(codes, codebooks, scales, x, y), ...] sharing (M, B)
+    in one launch; each y [d_out] is written in place.  Returns the y list."""
+    if not 1 <= len(problems) <= _lib.MAX_GROUPED:
+        raise ValueError(f"1..{_lib.MAX_GROUPED} problems per grouped launch")
+    arr = (_lib.GemvProblem * len(problems))()
+    fmt = None
+    for i, (codes, codebooks, scales, x, y) in enumerate(problems):
+        d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+        if fmt is None:
+            fmt = (M, B, g)
+        elif fmt != (M, B, g):
+            raise ValueError("grouped problems must share (M, B, g)")
+        if x.dtype != torch.float16 or x.numel() != d_in or not x.is_cuda or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
+        if y.dtype != torch.float16 or y.numel() != d_out or not y.is_cuda or not y.is_contiguous():
+            raise ValueError("y must be a contiguous fp16 GPU tensor with d_out elements")
+        arr[i] = _lib.GemvProblem(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), x.data_ptr(),
+                                  y.data_ptr(), d_out, d_in)
+    st = _lib.load().aqlm_gemv_grouped(arr, len(problems), fmt[0], fmt[1], fmt[2], _stream_handle(stream))
+    _check(st, "aqlm_gemv_grouped")
+    return [p[4] for p in problems]
 
 
 def gemm_small_batch(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:

@@ -17,7 +17,15 @@ LIB_PATH = os.path.join(HERE, "libaqlm_mi355x.so")
 AQLM_OK = 0
 STATUS_NAMES = {0: "AQLM_OK", 1: "AQLM_ERR_NULL", 2: "AQLM_ERR_SHAPE", 3: "AQLM_ERR_UNSUPPORTED",
                 4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP"}
-EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemm_small_batch", "aqlm_status_string")
+EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemm_small_batch", "aqlm_status_string")
+MAX_GROUPED = 8
+
+
+class GemvProblem(ctypes.Structure):
+    """Mirror of ``aqlm_gemv_problem`` in include/aqlm.h."""
+    _fields_ = [("codes", ctypes.c_void_p), ("codebooks", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("x", ctypes.c_void_p), ("y", ctypes.c_void_p), ("d_out", ctypes.c_int64),
+                ("d_in", ctypes.c_int64)]
 
 _lock = threading.Lock()
 _lib = None
@@ -47,6 +55,8 @@ def load():
         lib.aqlm_dequantize.restype = ctypes.c_int
         lib.aqlm_gemv.argtypes = [p, p, p, i64, i64, i32, i32, i32, p, p, p]
         lib.aqlm_gemv.restype = ctypes.c_int
+        lib.aqlm_gemv_grouped.argtypes = [ctypes.POINTER(GemvProblem), i32, i32, i32, i32, p]
+        lib.aqlm_gemv_grouped.restype = ctypes.c_int
         lib.aqlm_gemm_small_batch.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p]
         lib.aqlm_gemm_small_batch.restype = ctypes.c_int
         lib.aqlm_status_string.argtypes = [ctypes.c_int]

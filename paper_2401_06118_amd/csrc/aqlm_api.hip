@@ -54,6 +54,13 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
 
 int status_of(hipError_t e) { return e == hipSuccess ? AQLM_OK : AQLM_ERR_HIP; }
 
+// n = 1: the matrix-core kernel for M in {1, 2, 4} (B = 8) and 1x16; the
+// vector-ALU kernel for the other codebook counts.
+hipError_t gemv_dispatch(const aqlm::Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s) {
+  if (aqlm::gemv_mfma_supported(L.M, L.B)) return aqlm::launch_gemv_mfma(&L, &x, &y, 1, s);
+  return aqlm::launch_gemv(L, x, y, s);
+}
+
 }  // namespace
 
 extern "C" {
@@ -75,7 +82,7 @@ int aqlm_gemv(const void* codes, const uint16_t* codebooks, const uint16_t* scal
   if (st != AQLM_OK) return st;
   if (!x || !y) return AQLM_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
-  return status_of(aqlm::launch_gemv(L, x, y, static_cast<hipStream_t>(stream)));
+  return status_of(gemv_dispatch(L, x, y, static_cast<hipStream_t>(stream)));
 }
 
 int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
@@ -88,12 +95,39 @@ int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const ui
   if (n <= 0 || n >= (int64_t(1) << 31) || n * d_in >= (int64_t(1) << 40)) return AQLM_ERR_SHAPE;
   if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (n == 1) return status_of(aqlm::launch_gemv(L, x, y, s));
+  if (n == 1) return status_of(gemv_dispatch(L, x, y, s));
   if (aqlm::mfma_supported(L)) return status_of(aqlm::launch_gemm_mfma(L, (int32_t)n, x, y, s));
   // Formats the matrix-core kernel does not tile (M = 3, 5, 6, 7): one
   // matrix-vector launch per activation row.
   for (int64_t t = 0; t < n; ++t) {
-    const hipError_t e = aqlm::launch_gemv(L, x + t * d_in, y + t * d_out, s);
+    const hipError_t e = gemv_dispatch(L, x + t * d_in, y + t * d_out, s);
+    if (e != hipSuccess) return AQLM_ERR_HIP;
+  }
+  return AQLM_OK;
+}
+
+int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                      void* stream) {
+  if (!problems) return AQLM_ERR_NULL;
+  if (count < 1 || count > AQLM_MAX_GROUPED) return AQLM_ERR_SHAPE;
+  aqlm::Layer Ls[AQLM_MAX_GROUPED];
+  const uint16_t* xs[AQLM_MAX_GROUPED];
+  uint16_t* ys[AQLM_MAX_GROUPED];
+  for (int i = 0; i < count; ++i) {
+    const aqlm_gemv_problem& P = problems[i];
+    const int st = check_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &Ls[i]);
+    if (st != AQLM_OK) return st;
+    if (!P.x || !P.y) return AQLM_ERR_NULL;
+    if (!aligned(P.x, 16) || !aligned(P.y, 16)) return AQLM_ERR_ALIGN;
+    xs[i] = P.x;
+    ys[i] = P.y;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  bool same_class = true;
+  for (int i = 1; i < count; ++i) same_class = same_class && Ls[i].vec_codes == Ls[0].vec_codes;
+  if (aqlm::gemv_mfma_supported(M, B) && same_class) return status_of(aqlm::launch_gemv_mfma(Ls, xs, ys, count, s));
+  for (int i = 0; i < count; ++i) {
+    const hipError_t e = gemv_dispatch(Ls[i], xs[i], ys[i], s);
     if (e != hipSuccess) return AQLM_ERR_HIP;
   }
   return AQLM_OK;

@@ -1,0 +1,376 @@
+// Batch-1 AQLM matrix-vector product on the matrix cores (the token
+// generation product of Sec. 4.3):  y_i = fp16(s_i * sum_j sum_m <C_m[b_ijm], x_j>).
+//
+// v_mfma_f32_16x16x32_f16 takes, per lane, 8 consecutive K values of one row
+// of A (lane = row + 16 * K-slot) and 8 K values of one column of B (lane =
+// column + 16 * K-slot).  A lane's A fragment is one gathered codeword, so the
+// matrix core does the multiply-adds that a vector-ALU version would spend
+// v_dot2 instructions on, and it also sums over K, so no cross-lane reduction
+// is needed.  Only column 0 of B carries x (the other 15 columns read the same
+// LDS address and their outputs are ignored).
+//
+// Work split.  A workgroup (16 waves) owns a range of rows of one problem.  An
+// item is 16 rows x one K-slice of 4 x kCPL codes (kCPL = 16 codes, 16 bytes,
+// per lane); lane (r, s) streams the codes [s*kCPL, s*kCPL + kCPL) of the
+// slice for row r with one 16-byte load.  Each wave takes NI consecutive items
+// (rows-block major), keeps one accumulator per 16-row block and stores it to
+// LDS when its block changes; the partials are added in a fixed order at the
+// end, so results are deterministic.
+//
+// Memory order.  Vector-memory loads retire in issue order, so the small
+// loads that must finish first (codebooks, x) are issued before the HBM code
+// stream; all NI code loads of a wave are then in flight at once.  While
+// they arrive the codebooks are copied COPIES times into LDS (lane l reads
+// copy l % COPIES, so 16 lanes hit 16 different 16-byte bank quads) and x is
+// staged in LDS, zero-padded to whole K-slices.  B = 16 codebooks (1 MiB)
+// stay in L2 and are gathered with 16-byte global loads.
+//
+// Several independent problems with the same (M, B) can share one launch
+// (e.g. the q, k, v projections of a layer): workgroups are dealt to the
+// problems in proportion to their code bytes.
+#include "common.h"
+#include "launch.h"
+
+namespace aqlm {
+
+namespace {
+
+constexpr int kWaves = 16;
+constexpr int kThreads = kWaves * kWave;
+constexpr int kMaxRB = 8;  // 16-row blocks per workgroup
+
+template <int B>
+struct GCfg {
+  static constexpr int kBpc = B / 8;          // bytes per code
+  static constexpr int kCPL = 16 / kBpc;      // codes per lane per item
+  static constexpr int kKS = 4 * kCPL;        // codes per row per item
+  static constexpr int kXL = (B == 8) ? 4 : 8;  // x staging loads per thread (groups <= kXL * 1024)
+};
+
+// Generic (unaligned-pitch) path: byte loads of the valid codes of a lane's
+// 16-byte slot, zero past the row end.
+template <int B>
+__device__ __forceinline__ void load_codes_bytes(const uint8_t* __restrict__ row_ptr, uint32_t pitch, uint32_t off,
+                                                 uint32_t (&w)[4]) {
+  w[0] = w[1] = w[2] = w[3] = 0;
+  const int nbytes = off < pitch ? (int)min(pitch - off, 16u) : 0;
+#pragma unroll
+  for (int b = 0; b < 16; ++b)
+    if (b < nbytes) w[b / 4] |= (uint32_t)row_ptr[off + b] << (8 * (b % 4));
+}
+
+typedef __attribute__((address_space(3))) const u32x4_t lds_v4;
+
+// 16-byte LDS load from an LDS byte address (ds_read_b128).
+__device__ __forceinline__ uint4 lds_load16(uint32_t byte_addr) {
+  const u32x4_t v = *(lds_v4*)(uintptr_t)byte_addr;
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+// LDS byte address of codeword `code` of codebook m for this lane's copy.
+// With 16 copies and M <= 2 the address is (m << 16) | (code << 8) | (copy << 4),
+// built from the code byte with a single v_perm_b32: byte 0 and byte 2 come
+// from base_m = (m << 16) | (copy << 4), byte 1 is byte `k` of the code word.
+template <int M, int COPIES>
+__device__ __forceinline__ uint32_t cw_addr(uint32_t word, int k, uint32_t base_m, uint32_t copy_off, int m) {
+  if constexpr (COPIES == 16 && M <= 2) {
+    (void)copy_off;
+    (void)m;
+    return __builtin_amdgcn_perm(word, base_m, 0x0C020000u | ((uint32_t)(4 + k) << 8));
+  } else {
+    (void)base_m;
+    const uint32_t code = (word >> (8 * k)) & 0xFFu;
+    return ((uint32_t)(m * 256) + code) * (uint32_t)(COPIES * 16) + copy_off;
+  }
+}
+
+template <int M, int B, int COPIES, int PF, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
+  using C = GCfg<B>;
+  extern __shared__ uint4 lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  // wave-uniform: lets the item bookkeeping below run on the scalar unit
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int r16 = lane & 15;
+  const int slot = lane >> 4;
+
+  int p = 0;
+  while (p + 1 < bt.count && bt.p[p + 1].wg_begin <= (int)blockIdx.x) ++p;
+  const uint4* __restrict__ cb = bt.p[p].cb;
+  const uint4* __restrict__ x = bt.p[p].x;
+  const int32_t rows_per_wg = bt.p[p].rows_per_wg;
+  const int32_t row0 = ((int32_t)blockIdx.x - bt.p[p].wg_begin) * rows_per_wg;
+  int32_t rows = bt.p[p].d_out - row0;
+  if (rows > rows_per_wg) rows = rows_per_wg;
+  const int RB = (rows + 15) / 16;
+  const int32_t G = bt.p[p].G;
+  const uint32_t pitch = (uint32_t)G * M * C::kBpc;     // code bytes per row
+  const int KS = (int)((pitch + 63u) / 64u);             // 64-byte K-slices per row (4 slots x 16 bytes)
+  const int items = RB * KS;
+  const int xg = KS * (C::kKS / M);  // x groups staged (zero past G)
+  // Items are dealt round-robin: wave w takes items w, w + 16, w + 32, ...
+  // (nk of them); item i covers row block i / KS and K-slice i % KS.
+  const int nk = items > wave ? (items - wave + kWaves - 1) / kWaves : 0;
+  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * pitch;
+
+  constexpr int kCbEntries = (B == 8) ? M * 256 * COPIES : 0;
+  uint4* cb_lds = lds;
+  uint4* x_lds = lds + kCbEntries;
+  float* part = reinterpret_cast<float*>(x_lds + bt.xg_max);
+
+  // 1. small loads first (codebooks, x): vector-memory loads retire in issue
+  // order, so these complete without waiting for the HBM code stream.
+  uint4 cbv = make_uint4(0, 0, 0, 0);
+  if constexpr (B == 8) {
+    if (tid < M * 256) cbv = cb[tid];
+  }
+  uint4 xv[C::kXL];
+#pragma unroll
+  for (int i = 0; i < C::kXL; ++i) {
+    const int grp = tid + i * kThreads;
+    xv[i] = make_uint4(0, 0, 0, 0);
+    if (grp < G) xv[i] = x[grp];
+  }
+
+  // 2. the first PF items of the code stream.  The prefetch cursor stops at
+  // the wave's last item, so loads past the end repeat that item (valid
+  // memory; their results are never used).
+  const uint32_t slot_off = (uint32_t)slot * 16u;
+  auto issue = [&](int rb, int ks, uint32_t (&w)[4]) {
+    int row = rb * 16 + r16;
+    row = row < rows ? row : rows - 1;
+    const uint32_t off = (uint32_t)ks * 64u + slot_off;
+    if constexpr (VEC) {
+      // a 16-byte slot is wholly inside the row or wholly past its end
+      const uint32_t o = (uint32_t)row * pitch + (off < pitch ? off : 0u);
+      const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
+      w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
+    } else {
+      load_codes_bytes<B>(wg_codes + (size_t)row * pitch, pitch, off, w);
+    }
+  };
+  auto advance = [&](int& rb, int& ks) {
+    ks += kWaves;
+    while (ks >= KS) { ks -= KS; ++rb; }
+  };
+  int f_rb = nk > 0 ? wave / KS : 0, f_ks = nk > 0 ? wave % KS : 0, f_k = 0;
+  uint32_t buf[PF][4];
+#pragma unroll
+  for (int u = 0; u < PF; ++u) {
+    issue(f_rb, f_ks, buf[u]);
+    if (f_k + 1 < nk) advance(f_rb, f_ks);
+    ++f_k;
+  }
+
+  // 3. stage codebook copies, x and zeroed partials in LDS.
+  if constexpr (B == 8) {
+    if (tid < M * 256) {
+#pragma unroll
+      for (int k = 0; k < COPIES; ++k) cb_lds[tid * COPIES + ((k + lane) % COPIES)] = cbv;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < C::kXL; ++i) {
+    const int grp = tid + i * kThreads;
+    if (grp < xg) x_lds[grp] = xv[i];
+  }
+  for (int e = tid; e < RB * kWaves * 16; e += kThreads) part[e] = 0.f;
+  __syncthreads();
+
+  // 4. stream the items: gather codewords (A), x from LDS (B), MFMA.
+  const uint32_t copy_off = (uint32_t)(lane % (COPIES > 0 ? COPIES : 1)) * 16u;
+  // LDS byte address of the codebook copies (low 32 bits of the flat address
+  // of an LDS object are its LDS offset)
+  const uint32_t cb_base = (uint32_t)(uintptr_t)cb_lds;
+  uint32_t base_m[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) base_m[m] = cb_base + ((uint32_t)m << 16) + copy_off;
+  f4_t acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};  // even / odd steps
+  // B operand: only column 0 (lanes with r16 == 0) carries x; the other
+  // columns keep whatever they hold and their outputs are never read.
+  uint4 xb = make_uint4(0, 0, 0, 0);
+  int cur_rb = -1;
+  int c_rb = nk > 0 ? wave / KS : 0, c_ks = nk > 0 ? wave % KS : 0;
+  for (int k0 = 0; k0 < nk; k0 += PF) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+      const int k = k0 + u;
+      const uint32_t cw[4] = {buf[u][0], buf[u][1], buf[u][2], buf[u][3]};
+      uint4 av[C::kCPL];
+      if constexpr (B == 16) {
+        // L2 gathers go out before the next code load so that waiting for
+        // them does not wait for HBM.
+        if (k < nk) {
+#pragma unroll
+          for (int t = 0; t < C::kCPL; ++t)
+            av[t] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb) +
+                                                     (((cw[t / 2] >> (16 * (t % 2))) & 0xFFFFu) << 4));
+        }
+      }
+      issue(f_rb, f_ks, buf[u]);
+      if (f_k + 1 < nk) advance(f_rb, f_ks);
+      ++f_k;
+      if (k < nk) {
+        if (c_rb != cur_rb) {
+          if (cur_rb >= 0 && r16 == 0) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) part[(cur_rb * kWaves + wave) * 16 + 4 * slot + e] = acc[e] + acc2[e];
+          }
+          acc = f4_t{0.f, 0.f, 0.f, 0.f};
+          acc2 = f4_t{0.f, 0.f, 0.f, 0.f};
+          cur_rb = c_rb;
+        }
+        // x groups of this lane's codes; past the row end x is zero
+        const uint4* xs = x_lds + (((uint32_t)c_ks * C::kKS + (uint32_t)slot * C::kCPL) / M);
+#pragma unroll
+        for (int t0 = 0; t0 < C::kCPL; t0 += 4) {
+          if constexpr (B == 8) {
+#pragma unroll
+            for (int uu = 0; uu < 4; ++uu) {
+              const int t = t0 + uu;
+              const uint32_t addr = cw_addr<M, COPIES>(cw[t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M);
+              av[t] = lds_load16(addr);
+            }
+          }
+#pragma unroll
+          for (int uu = 0; uu < 4; ++uu) {
+            const int t = t0 + uu;
+            if (t % M == 0 || uu == 0) {  // codes t .. t+M-1 share the group t/M of the slot
+              if (r16 == 0) xb = xs[t / M];
+            }
+            f4_t& a = (uu % 2 == 0) ? acc : acc2;
+            a = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[t]), __builtin_bit_cast(h8_t, xb),
+                                                      a, 0, 0, 0);
+          }
+        }
+        advance(c_rb, c_ks);
+      }
+    }
+  }
+  if (cur_rb >= 0 && r16 == 0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) part[(cur_rb * kWaves + wave) * 16 + 4 * slot + e] = acc[e] + acc2[e];
+  }
+  __syncthreads();
+
+  // 5. fixed-order sum over waves, scale, round, store.
+  if (tid < rows) {
+    const int rb = tid / 16, rr = tid % 16;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += part[(rb * kWaves + w) * 16 + rr];
+    bt.p[p].y[row0 + tid] = f2h(h2f(bt.p[p].scales[row0 + tid]) * s);
+  }
+}
+
+template <int M, int B, int COPIES, int PF, bool VEC>
+hipError_t launch_pf(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
+  auto kern = k_gemv_mfma<M, B, COPIES, PF, VEC>;
+  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(bt.total_wgs), dim3(kThreads), lds_bytes, s, bt);
+  return hipGetLastError();
+}
+
+template <int M, int B, int COPIES, bool VEC>
+hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStream_t s) {
+  switch (pf) {
+    case 1: return launch_pf<M, B, COPIES, 1, VEC>(bt, lds_bytes, s);
+    case 2: return launch_pf<M, B, COPIES, 2, VEC>(bt, lds_bytes, s);
+    case 4: return launch_pf<M, B, COPIES, 4, VEC>(bt, lds_bytes, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool gemv_mfma_supported(int M, int B) { return (B == 16 && M == 1) || (B == 8 && (M == 1 || M == 2 || M == 4)); }
+
+// Deal workgroups to problems, pick rows per workgroup and items per wave,
+// size LDS, and launch.  All problems share (M, B) and the code-pitch
+// alignment class.
+hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
+                            hipStream_t s) {
+  if (count < 1 || count > kMaxProblems) return hipErrorInvalidValue;
+  const int M = Ls[0].M, B = Ls[0].B;
+  const int kCPL = (B == 8) ? 16 : 8, kKS = 4 * kCPL;
+  bool vec = true;
+  double total_bytes = 0;
+  for (int i = 0; i < count; ++i) {
+    vec = vec && Ls[i].vec_codes;
+    total_bytes += (double)Ls[i].d_out * Ls[i].G * M * (B / 8);
+  }
+  const int cus = num_cus();
+  GemvBatch bt{};
+  bt.count = count;
+  int wg = 0, ni_max = 1, xg_max = 0, rb_max = 1;
+  for (int i = 0; i < count; ++i) {
+    const Layer& L = Ls[i];
+    const double bytes = (double)L.d_out * L.G * M * (B / 8);
+    int want = (int)(cus * bytes / total_bytes + 0.5);
+    if (want < 1) want = 1;
+    int rows_per_wg = (L.d_out + want - 1) / want;
+    const int64_t cpr = (int64_t)L.G * M;
+    const int KS = (int)((cpr + kKS - 1) / kKS);
+    // at most kMaxRB row blocks per workgroup (partial-sum space in LDS);
+    // larger layers get more workgroups than CUs
+    if (rows_per_wg > kMaxRB * 16) rows_per_wg = kMaxRB * 16;
+    const int nwg = (L.d_out + rows_per_wg - 1) / rows_per_wg;
+    const int rb = (rows_per_wg + 15) / 16;
+    const int ni = (rb * KS + kWaves - 1) / kWaves;
+    GemvProblem& P = bt.p[i];
+    P.codes = static_cast<const uint8_t*>(L.codes);
+    P.cb = reinterpret_cast<const uint4*>(L.codebooks);
+    P.scales = L.scales;
+    P.x = reinterpret_cast<const uint4*>(xs[i]);
+    P.y = ys[i];
+    P.d_out = L.d_out;
+    P.G = L.G;
+    P.wg_begin = wg;
+    P.rows_per_wg = rows_per_wg;
+    wg += nwg;
+    if (ni > ni_max) ni_max = ni;
+    const int xg = KS * (kKS / M);
+    if (xg > xg_max) xg_max = xg;
+    if (rb > rb_max) rb_max = rb;
+  }
+  bt.total_wgs = wg;
+  bt.xg_max = xg_max;
+  const int ni = ni_max <= 1 ? 1 : (ni_max == 2 ? 2 : 4);  // prefetch depth
+  const int xl = (B == 8) ? 4 : 8;
+  if (xg_max > xl * kThreads) return hipErrorInvalidValue;
+  const size_t base = (size_t)xg_max * 16 + (size_t)rb_max * kWaves * 16 * 4;
+  const size_t limit = 160 * 1024;
+  if (B == 16) {
+    if (base > limit) return hipErrorInvalidValue;
+    return vec ? launch_copies<1, 16, 0, true>(bt, ni, base, s) : launch_copies<1, 16, 0, false>(bt, ni, base, s);
+  }
+  // the most codebook copies that fit next to x and the partials
+  const size_t per_copy = (size_t)M * 256 * 16;
+  int copies = 16;
+  while (copies > 1 && base + per_copy * copies > limit) copies /= 2;
+  if (base + per_copy * copies > limit) return hipErrorInvalidValue;
+  const size_t lds = base + per_copy * copies;
+#define AQLM_GEMV_COPIES(MM)                                                                            \
+  switch (copies) {                                                                                     \
+    case 16: return vec ? launch_copies<MM, 8, 16, true>(bt, ni, lds, s) : launch_copies<MM, 8, 16, false>(bt, ni, lds, s); \
+    case 8: return vec ? launch_copies<MM, 8, 8, true>(bt, ni, lds, s) : launch_copies<MM, 8, 8, false>(bt, ni, lds, s);     \
+    case 4: return vec ? launch_copies<MM, 8, 4, true>(bt, ni, lds, s) : launch_copies<MM, 8, 4, false>(bt, ni, lds, s);     \
+    default: return hipErrorInvalidValue;                                                               \
+  }
+  switch (M) {
+    case 1: AQLM_GEMV_COPIES(1)
+    case 2: AQLM_GEMV_COPIES(2)
+    case 4: AQLM_GEMV_COPIES(4)
+  }
+#undef AQLM_GEMV_COPIES
+  return hipErrorInvalidValue;
+}
+
+}  // namespace aqlm

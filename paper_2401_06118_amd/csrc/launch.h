@@ -20,7 +20,33 @@ struct Layer {
   bool vec_codes;  // codes base 16-byte aligned and row pitch a multiple of 16 bytes
 };
 
+constexpr int kMaxProblems = 8;
+
+// One matrix-vector problem of a (possibly grouped) launch and its share of
+// the workgroups: workgroups [wg_begin, wg_begin + ceil(d_out / rows_per_wg)).
+struct GemvProblem {
+  const uint8_t* codes;
+  const uint4* cb;
+  const uint16_t* scales;
+  const uint4* x;  // [G] groups of 8 fp16
+  uint16_t* y;
+  int32_t d_out;
+  int32_t G;
+  int32_t wg_begin;
+  int32_t rows_per_wg;
+};
+
+struct GemvBatch {
+  GemvProblem p[kMaxProblems];
+  int32_t count;
+  int32_t total_wgs;
+  int32_t xg_max;  // x groups staged in LDS by the largest problem
+};
+
 hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s);
+bool gemv_mfma_supported(int M, int B);
+hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
+                            hipStream_t s);
 hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s);
 hipError_t launch_gemm_mfma(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
 bool mfma_supported(const Layer& L);

@@ -88,3 +88,24 @@ def special_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, 
     codes = rng.integers(0, entries, size=(d_out, d_in // g, M), dtype=code_dtype(B))
     x = rng.standard_normal((n, d_in)).astype(np.float16)
     return Layer(codes, codebooks, scales, x, M, B, g)
+
+
+def device_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, n: int = 1,
+                 device="cuda", cb_std: float = 0.02):
+    """The same distributions drawn on the GPU with torch's seeded generator
+    (for multi-GiB benchmark workloads; the bytes differ from :func:`layer`).
+    Returns (codes, codebooks, scales, x) as torch tensors on ``device``;
+    codes are uint8 (B <= 8) or int16 holding uint16 bit patterns (B = 16)."""
+    import torch
+
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    if B <= 8:
+        codes = torch.randint(0, 1 << B, (d_out, d_in // g, M), dtype=torch.uint8, device=device, generator=gen)
+    else:
+        codes = torch.randint(-(1 << 15), 1 << 15, (d_out, d_in // g, M), dtype=torch.int16, device=device,
+                              generator=gen)
+    codebooks = (torch.randn((M, 1 << B, g), device=device, generator=gen) * cb_std).to(torch.float16)
+    scales = torch.empty(d_out, device=device).uniform_(0.5, 1.5, generator=gen).to(torch.float16)
+    x = torch.randn((n, d_in), device=device, generator=gen).to(torch.float16)
+    return codes, codebooks, scales, x

@@ -112,3 +112,19 @@ def test_binding_refuses_cpu_tensors():
     sc = torch.ones(4, dtype=torch.float16)
     with pytest.raises(ValueError):
         aq.dequantize(codes, cb, sc)
+
+
+def test_grouped_validation(lib):
+    Prob = _lib.GemvProblem
+    good = Prob(P, P, P, P, P, 64, 64)
+    arr = (Prob * 9)(*([good] * 9))
+    assert lib.aqlm_gemv_grouped(None, 1, 2, 8, 8, None) == NULL
+    assert lib.aqlm_gemv_grouped(arr, 0, 2, 8, 8, None) == SHAPE
+    assert lib.aqlm_gemv_grouped(arr, 9, 2, 8, 8, None) == SHAPE
+    assert lib.aqlm_gemv_grouped(arr, 2, 2, 16, 8, None) == UNSUP
+    bad = (Prob * 3)(good, Prob(P, P, P, P, P, 64, 60), good)
+    assert lib.aqlm_gemv_grouped(bad, 3, 2, 8, 8, None) == SHAPE
+    bad = (Prob * 2)(good, Prob(P, P, P, None, P, 64, 64))
+    assert lib.aqlm_gemv_grouped(bad, 2, 2, 8, 8, None) == NULL
+    bad = (Prob * 2)(good, Prob(P, P, P, P + 2, P, 64, 64))
+    assert lib.aqlm_gemv_grouped(bad, 2, 2, 8, 8, None) == ALIGN

@@ -222,3 +222,57 @@ def test_argument_errors_leave_outputs_untouched():
     assert st == 4
     torch.cuda.synchronize()
     assert torch.all(y == 7.0)
+
+
+# ------------------------------------------------------------- grouped launch
+
+def _grouped_case(shapes, M, B, seed):
+    lays = [synth.layer(seed + 31 * i, d_out, d_in, M, B) for i, (d_out, d_in) in enumerate(shapes)]
+    probs, ys = [], []
+    for lay in lays:
+        codes, cb, sc, x = to_device(lay)
+        y = torch.full((lay.d_out,), float("nan"), dtype=torch.float16, device="cuda")
+        probs.append((codes, cb, sc, x[0], y))
+        ys.append(y)
+    aq().gemv_grouped(probs)
+    torch.cuda.synchronize()
+    for lay, y in zip(lays, ys):
+        check_products(lay, fp16_to_np(y)[None, :])
+    return probs
+
+
+@pytest.mark.parametrize("shapes,M,B", [
+    ([(4096, 4096)] * 3, 2, 8),                        # q, k, v
+    ([(11008, 4096)] * 2, 2, 8),                       # gate, up
+    ([(4096, 4096)] * 3, 1, 16),
+    ([(1000, 4104), (64, 512), (3000, 2048), (17, 8)], 2, 8),
+    ([(1024, 8192), (1024, 8192), (8192, 8192)], 4, 8),
+    ([(256, 1024)] * 8, 1, 8),
+    ([(100, 520), (37, 1040)], 3, 8),                  # format without the matrix-core path
+])
+def test_gemv_grouped_matches_oracle(shapes, M, B):
+    print(f"[grouped] {shapes} M={M} B={B}", flush=True)
+    _grouped_case(shapes, M, B, 8000 + M)
+
+
+def test_gemv_grouped_deterministic():
+    probs = _grouped_case([(4096, 4096)] * 3, 2, 8, 8100)
+    first = [p[4].cpu().numpy().view(np.uint16).copy() for p in probs]
+    aq().gemv_grouped(probs)
+    again = [p[4].cpu().numpy().view(np.uint16) for p in probs]
+    assert all(np.array_equal(a, b) for a, b in zip(first, again))
+
+
+def test_gemv_grouped_error_writes_nothing():
+    lay = synth.layer(8200, 64, 64, 2, 8)
+    codes, cb, sc, x = to_device(lay)
+    y0 = torch.full((64,), 5.0, dtype=torch.float16, device="cuda")
+    y1 = torch.full((64,), 5.0, dtype=torch.float16, device="cuda")
+    import paper_2401_06118_amd._lib as L
+    arr = (L.GemvProblem * 2)(L.GemvProblem(codes.data_ptr(), cb.data_ptr(), sc.data_ptr(), x.data_ptr(),
+                                            y0.data_ptr(), 64, 64),
+                              L.GemvProblem(codes.data_ptr(), cb.data_ptr(), sc.data_ptr(), x.data_ptr(),
+                                            y1.data_ptr(), 64, 60))
+    assert L.load().aqlm_gemv_grouped(arr, 2, 2, 8, 8, None) == 2
+    torch.cuda.synchronize()
+    assert torch.all(y0 == 5.0) and torch.all(y1 == 5.0)
