@@ -11,8 +11,12 @@ measured step time; tokens/s-equivalent is 1 / step time (linear layers only:
 attention, norms, embeddings and the LM head are not part of the step).
 
 Also reported on the same JSON line:
-  roofline      the dominant kernel (the matrix-vector kernel) against 8 TB/s,
-                with its average duration from HIP events around each launch;
+  roofline      the dominant kernel (the matrix-vector kernel) against 8 TB/s:
+                algorithmic bytes per launch over its average launch duration,
+                the event-timed replay region divided by the launches in it;
+                ``traffic`` is the HBM bytes per launch that the committed
+                rocprofv3 counter summary records for this kernel source
+                (null once the source has changed);
   cpu_baseline  the CPU oracle (dequantize + fp64 product) timed on the host
                 cores on a sample of the step's layers, scaled to the step;
   secondary     the same step in the 1x16 scheme, single layers rotated over
@@ -58,6 +62,9 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device copy a few times (the reference kernel for "
+                         "scaling HBM byte counters) and exit")
     return ap.parse_args()
 
 
@@ -167,10 +174,16 @@ def per_launch_ms(launches, reps):
 
 
 def source_digest(*names):
+    """Digest of kernel sources with comments and whitespace removed, so that
+    it changes with the code and not with its comments."""
+    import re
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(ROOT, "paper_2401_06118_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2401_06118_amd", "csrc", n), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update("".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -286,12 +299,40 @@ def batch_rows(aq, torch):
     return rows
 
 
+def kernel_name(M: int, B: int) -> str:
+    """Device kernel that serves a batch-1 product of this format."""
+    if B == 8 and M in (1, 2, 4):
+        return "aqlm::k_gemv_ks"
+    if B == 16 and M == 1:
+        return "aqlm::k_gemv_mfma"
+    return "aqlm::k_gemv"
+
+
+COPY_BYTES = 256 << 20
+
+
+def copy_calibration():
+    """A plain device-to-device copy of known size: it reads and writes
+    COPY_BYTES once per launch, so HBM byte counters taken on it give the
+    scale between counter readings and bytes moved."""
+    import torch
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "launches": 5}), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
               "(no multi-GPU path exists).", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
 
     import paper_2401_06118_amd as aq
@@ -308,14 +349,14 @@ def main():
     log(f"step {ms:.4f} ms (graph replay)")
 
     # Dominant kernel: every launch of the step is the matrix-vector kernel
-    # (grouped or single); its average duration from an event pair per launch.
-    kern = per_launch_ms(launches, reps=max(2, min(args.steps, 5)))
-    kern_total_ms = sum(kern)
-    avg_launch_ms = kern_total_ms / len(launches)
+    # (grouped or single), so its average launch duration is the graph-timed
+    # region (HIP events on the replay stream) divided by the launches in it.
+    avg_launch_ms = ms / len(launches)
     bytes_per_launch = step_bytes / len(launches)
     achieved = bytes_per_launch / (avg_launch_ms * 1e6)
     digest = source_digest("gemv_mfma.hip", "common.h")
-    traffic = measured_traffic(f"gemv_{model}_{M}x{B}", digest)
+    kname = kernel_name(M, B)
+    traffic = measured_traffic(f"{kname}:{args.workload}", digest)
 
     result = {
         "metric": "achieved HBM GB/s & roofline % for AQLM GEMV (batch 1); decode tokens/s-equivalent",
@@ -341,11 +382,9 @@ def main():
         },
         "tokens_per_s_equivalent": 1000.0 / ms,
         "roofline_frac_step": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
-        "kernel_only": {"sum_kernel_ms": kern_total_ms, "GBs": step_bytes / (kern_total_ms * 1e6),
-                        "tok_s_eq": 1000.0 / kern_total_ms},
         "roofline": {
             "bound": "hbm",
-            "kernel": f"k_gemv_mfma<M={M},B={B}>",
+            "kernel": kname,
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",

@@ -12,10 +12,13 @@
 // Work split.  A workgroup (16 waves) owns a range of rows of one problem.  An
 // item is 16 rows x one K-slice of 4 x kCPL codes (kCPL = 16 codes, 16 bytes,
 // per lane); lane (r, s) streams the codes [s*kCPL, s*kCPL + kCPL) of the
-// slice for row r with one 16-byte load.  Each wave takes NI consecutive items
-// (rows-block major), keeps one accumulator per 16-row block and stores it to
-// LDS when its block changes; the partials are added in a fixed order at the
-// end, so results are deterministic.
+// slice for row r with one 16-byte load.  Two schedules of the items:
+//   k_gemv_mfma (B = 16): items dealt round-robin to the waves, one
+//     accumulator per wave, stored to LDS whenever its row block changes;
+//   k_gemv_ks (B = 8): each wave owns whole K-slices of all the workgroup's
+//     row blocks and keeps one accumulator per block.
+// Either way the per-wave partials are added in a fixed order at the end, so
+// results are deterministic.
 //
 // Memory order.  Vector-memory loads retire in issue order, so the small
 // loads that must finish first (codebooks, x) are issued before the HBM code
@@ -264,6 +267,240 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
   }
 }
 
+// B = 8 variant, K-slice major.  Wave w owns the K-slices ks = w, w + 16, ...
+// of the workgroup's RB row blocks.  For each of its K-slices it reads the
+// x slices of its four code slots once into registers (column-0 lanes
+// only), then runs the RB items (row blocks) of that slice, each into its own
+// accumulator, so no partial sums move until the end.  Code loads run D
+// K-slices ahead (D * RB items, about four).
+template <int M, int COPIES, int RB, int D, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
+  using C = GCfg<8>;
+  constexpr int kXS = C::kCPL / M;  // x slices per code slot per K-slice
+  constexpr int kStep = RB >= 5 ? 2 : 4;  // codewords gathered per block before their MFMAs
+  extern __shared__ uint4 lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int r16 = lane & 15;
+  const int slot = lane >> 4;
+
+  int p = 0;
+  while (p + 1 < bt.count && bt.p[p + 1].wg_begin <= (int)blockIdx.x) ++p;
+  const uint4* __restrict__ cb = bt.p[p].cb;
+  const uint4* __restrict__ x = bt.p[p].x;
+  const int32_t rows_per_wg = bt.p[p].rows_per_wg;
+  const int32_t row0 = ((int32_t)blockIdx.x - bt.p[p].wg_begin) * rows_per_wg;
+  int32_t rows = bt.p[p].d_out - row0;
+  if (rows > rows_per_wg) rows = rows_per_wg;
+  const int32_t G = bt.p[p].G;
+  const uint32_t pitch = (uint32_t)G * M;           // code bytes per row
+  const int KS = (int)((pitch + 63u) / 64u);        // 64-byte K-slices per row
+  const int xg = KS * (C::kKS / M);
+  const int nks = KS > wave ? (KS - wave + kWaves - 1) / kWaves : 0;
+  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * pitch;
+
+  uint4* cb_lds = lds;
+  uint4* x_lds = lds + M * 256 * COPIES;
+  float* part = reinterpret_cast<float*>(x_lds + bt.xg_max);
+
+  // 1. codebooks and x first (they retire before the code stream).
+  uint4 cbv = make_uint4(0, 0, 0, 0);
+  if (tid < M * 256) cbv = cb[tid];
+  uint4 xv[C::kXL];
+#pragma unroll
+  for (int i = 0; i < C::kXL; ++i) {
+    const int grp = tid + i * kThreads;
+    xv[i] = make_uint4(0, 0, 0, 0);
+    if (grp < G) xv[i] = x[grp];
+  }
+
+  // 2. code loads for the first D K-slices (rows past the end repeat the last
+  // row; K-slices past the wave's last repeat that slice; never used).
+  const uint32_t slot_off = (uint32_t)slot * 16u;
+  int row_off[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = rb * 16 + r16;
+    row_off[rb] = (row < rows ? row : rows - 1) * (int)pitch;
+  }
+  auto issue = [&](int j, uint32_t (&w)[RB][4]) {
+    const int jj = j < nks ? j : (nks > 0 ? nks - 1 : 0);
+    const uint32_t off = (uint32_t)(wave + jj * kWaves) * 64u + slot_off;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      if constexpr (VEC) {
+        const uint32_t o = (uint32_t)row_off[rb] + (off < pitch ? off : 0u);
+        const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
+        w[rb][0] = v[0]; w[rb][1] = v[1]; w[rb][2] = v[2]; w[rb][3] = v[3];
+      } else {
+        load_codes_bytes<8>(wg_codes + row_off[rb], pitch, off, w[rb]);
+      }
+    }
+  };
+  auto issue_rb = [&](int j, int rb, uint32_t (&w)[4]) {
+    const int jj = j < nks ? j : (nks > 0 ? nks - 1 : 0);
+    const uint32_t off = (uint32_t)(wave + jj * kWaves) * 64u + slot_off;
+    if constexpr (VEC) {
+      const uint32_t o = (uint32_t)row_off[rb] + (off < pitch ? off : 0u);
+      const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
+      w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
+    } else {
+      load_codes_bytes<8>(wg_codes + row_off[rb], pitch, off, w);
+    }
+  };
+  uint32_t ring[D][RB][4];
+#pragma unroll
+  for (int d = 0; d < D; ++d) issue(d, ring[d]);
+
+  // 3. stage codebook copies, x and zeroed partials.
+  if (tid < M * 256) {
+#pragma unroll
+    for (int k = 0; k < COPIES; ++k) cb_lds[tid * COPIES + ((k + lane) % COPIES)] = cbv;
+  }
+#pragma unroll
+  for (int i = 0; i < C::kXL; ++i) {
+    const int grp = tid + i * kThreads;
+    if (grp < xg) x_lds[grp] = xv[i];
+  }
+  for (int e = tid; e < RB * kWaves * 16; e += kThreads) part[e] = 0.f;
+  __syncthreads();
+
+  // 4. K-slices of this wave.
+  const uint32_t copy_off = (uint32_t)(lane % COPIES) * 16u;
+  const uint32_t cb_base = (uint32_t)(uintptr_t)cb_lds;
+  uint32_t base_m[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) base_m[m] = cb_base + ((uint32_t)m << 16) + copy_off;
+  f4_t acc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) acc[rb] = f4_t{0.f, 0.f, 0.f, 0.f};
+  f4_t acc_odd = {0.f, 0.f, 0.f, 0.f};  // second chain of an unpaired last block
+  uint4 xr[kXS];
+#pragma unroll
+  for (int s2 = 0; s2 < kXS; ++s2) xr[s2] = make_uint4(0, 0, 0, 0);
+
+  const int rb_live = (rows + 15) / 16;  // row blocks this workgroup really has (<= RB)
+  for (int j0 = 0; j0 < nks; j0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int j = j0 + d;
+      if (j < nks) {
+        const int ks = wave + j * kWaves;
+        if (r16 == 0) {
+          const uint4* xs = x_lds + (((uint32_t)ks * C::kKS + (uint32_t)slot * C::kCPL) / M);
+#pragma unroll
+          for (int s2 = 0; s2 < kXS; ++s2) xr[s2] = xs[s2];
+        }
+      }
+      // Row blocks two at a time, their MFMAs interleaved so that two
+      // accumulation chains are in flight; a lone block alternates two
+      // accumulators.  Each block's codes are reloaded for K-slice j + D as
+      // soon as they are consumed.
+#pragma unroll
+      for (int rb = 0; rb < RB; rb += 2) {
+        const bool pair = rb + 1 < RB;
+        const bool live = j < nks && rb < rb_live;
+        const bool live2 = pair && j < nks && rb + 1 < rb_live;
+        if (live) {
+#pragma unroll
+          for (int t0 = 0; t0 < C::kCPL; t0 += kStep) {
+            uint4 av[kStep], bv[kStep];
+#pragma unroll
+            for (int u = 0; u < kStep; ++u) {
+              const int t = t0 + u;
+              av[u] = lds_load16(
+                  cw_addr<M, COPIES>(ring[d][rb][t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M));
+              if (pair)
+                bv[u] = lds_load16(
+                    cw_addr<M, COPIES>(ring[d][pair ? rb + 1 : rb][t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M));
+            }
+#pragma unroll
+            for (int u = 0; u < kStep; ++u) {
+              const int t = t0 + u;
+              const h8_t xh = __builtin_bit_cast(h8_t, xr[t / M]);
+              if (pair) {
+                acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, acc[rb], 0, 0, 0);
+                if (live2)
+                  acc[pair ? rb + 1 : rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                      __builtin_bit_cast(h8_t, bv[u]), xh, acc[pair ? rb + 1 : rb], 0, 0, 0);
+              } else {
+                f4_t& a = (u % 2 == 0) ? acc[rb] : acc_odd;
+                a = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, a, 0, 0, 0);
+              }
+            }
+          }
+        }
+        issue_rb(j + D, rb, ring[d][rb]);
+        if (pair) issue_rb(j + D, rb + 1, ring[d][pair ? rb + 1 : rb]);
+      }
+    }
+  }
+  if constexpr (RB % 2 == 1) acc[RB - 1] += acc_odd;
+  if (r16 == 0) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) part[(rb * kWaves + wave) * 16 + 4 * slot + e] = acc[rb][e];
+  }
+  __syncthreads();
+
+  // 5. fixed-order sum over waves, scale, round, store.
+  if (tid < rows) {
+    const int rb = tid / 16, rr = tid % 16;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += part[(rb * kWaves + w) * 16 + rr];
+    bt.p[p].y[row0 + tid] = f2h(h2f(bt.p[p].scales[row0 + tid]) * s);
+  }
+}
+
+template <int M, int COPIES, int RB, int D, bool VEC>
+hipError_t launch_ks(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
+  auto kern = k_gemv_ks<M, COPIES, RB, D, VEC>;
+  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3(bt.total_wgs), dim3(kThreads), lds_bytes, s, bt);
+  return hipGetLastError();
+}
+
+// Row blocks per workgroup the K-slice kernel keeps in registers without
+// spilling (1024 threads: 128 VGPRs per lane); M = 1 holds 16 x slices.
+constexpr int ks_rb_cap(int M) { return M == 1 ? 2 : 7; }
+
+// Code-load lookahead in K-slices: about four items, but never more
+// K-slices than a wave owns (extra loads would only repeat its last one).
+template <int M, int COPIES, int RB, bool VEC>
+hipError_t launch_ks_d(const GemvBatch& bt, int nks, size_t lds_bytes, hipStream_t s) {
+  constexpr int D4 = RB >= 4 ? 1 : (RB == 1 ? 4 : 2);
+  if (D4 >= 4 && nks >= 4) return launch_ks<M, COPIES, RB, (D4 >= 4 ? 4 : 1), VEC>(bt, lds_bytes, s);
+  if (D4 >= 2 && nks >= 2) return launch_ks<M, COPIES, RB, (D4 >= 2 ? 2 : 1), VEC>(bt, lds_bytes, s);
+  return launch_ks<M, COPIES, RB, 1, VEC>(bt, lds_bytes, s);
+}
+
+template <int M, int COPIES, bool VEC>
+hipError_t launch_ks_rb(const GemvBatch& bt, int rb, int nks, size_t lds_bytes, hipStream_t s) {
+  switch (rb) {
+    case 1: return launch_ks_d<M, COPIES, 1, VEC>(bt, nks, lds_bytes, s);
+    case 2: return launch_ks_d<M, COPIES, 2, VEC>(bt, nks, lds_bytes, s);
+  }
+  if constexpr (ks_rb_cap(M) >= 7) {
+    switch (rb) {
+      case 3: return launch_ks_d<M, COPIES, 3, VEC>(bt, nks, lds_bytes, s);
+      case 4: return launch_ks_d<M, COPIES, 4, VEC>(bt, nks, lds_bytes, s);
+      case 5: return launch_ks_d<M, COPIES, 5, VEC>(bt, nks, lds_bytes, s);
+      case 6: return launch_ks_d<M, COPIES, 6, VEC>(bt, nks, lds_bytes, s);
+      case 7: return launch_ks_d<M, COPIES, 7, VEC>(bt, nks, lds_bytes, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
 template <int M, int B, int COPIES, int PF, bool VEC>
 hipError_t launch_pf(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
   auto kern = k_gemv_mfma<M, B, COPIES, PF, VEC>;
@@ -309,18 +546,21 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   const int cus = num_cus();
   GemvBatch bt{};
   bt.count = count;
-  int wg = 0, ni_max = 1, xg_max = 0, rb_max = 1;
+  int wg = 0, ni_max = 1, xg_max = 0, rb_max = 1, nks_min = 1 << 30;
   for (int i = 0; i < count; ++i) {
     const Layer& L = Ls[i];
     const double bytes = (double)L.d_out * L.G * M * (B / 8);
     int want = (int)(cus * bytes / total_bytes + 0.5);
     if (want < 1) want = 1;
-    int rows_per_wg = (L.d_out + want - 1) / want;
     const int64_t cpr = (int64_t)L.G * M;
     const int KS = (int)((cpr + kKS - 1) / kKS);
-    // at most kMaxRB row blocks per workgroup (partial-sum space in LDS);
-    // larger layers get more workgroups than CUs
-    if (rows_per_wg > kMaxRB * 16) rows_per_wg = kMaxRB * 16;
+    // At most rb_cap row blocks per workgroup (accumulator registers and
+    // partial-sum space).  Larger layers run `rounds` workgroups per CU,
+    // split evenly rather than leaving a short last round.
+    const int rb_cap = (B == 16) ? kMaxRB : ks_rb_cap(M);
+    const int blocks = (L.d_out + 15) / 16;
+    const int rounds = (blocks + rb_cap * want - 1) / (rb_cap * want);
+    const int rows_per_wg = (L.d_out + want * rounds - 1) / (want * rounds);
     const int nwg = (L.d_out + rows_per_wg - 1) / rows_per_wg;
     const int rb = (rows_per_wg + 15) / 16;
     const int ni = (rb * KS + kWaves - 1) / kWaves;
@@ -339,6 +579,8 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     const int xg = KS * (kKS / M);
     if (xg > xg_max) xg_max = xg;
     if (rb > rb_max) rb_max = rb;
+    const int nks = (KS + kWaves - 1) / kWaves;  // K-slices of the busiest wave
+    if (nks < nks_min) nks_min = nks;
   }
   bt.total_wgs = wg;
   bt.xg_max = xg_max;
@@ -357,12 +599,15 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   while (copies > 1 && base + per_copy * copies > limit) copies /= 2;
   if (base + per_copy * copies > limit) return hipErrorInvalidValue;
   const size_t lds = base + per_copy * copies;
-#define AQLM_GEMV_COPIES(MM)                                                                            \
-  switch (copies) {                                                                                     \
-    case 16: return vec ? launch_copies<MM, 8, 16, true>(bt, ni, lds, s) : launch_copies<MM, 8, 16, false>(bt, ni, lds, s); \
-    case 8: return vec ? launch_copies<MM, 8, 8, true>(bt, ni, lds, s) : launch_copies<MM, 8, 8, false>(bt, ni, lds, s);     \
-    case 4: return vec ? launch_copies<MM, 8, 4, true>(bt, ni, lds, s) : launch_copies<MM, 8, 4, false>(bt, ni, lds, s);     \
-    default: return hipErrorInvalidValue;                                                               \
+#define AQLM_GEMV_COPIES(MM)                                                                     \
+  switch (copies) {                                                                              \
+    case 16: return vec ? launch_ks_rb<MM, 16, true>(bt, rb_max, nks_min, lds, s)                        \
+                        : launch_ks_rb<MM, 16, false>(bt, rb_max, nks_min, lds, s);                      \
+    case 8: return vec ? launch_ks_rb<MM, 8, true>(bt, rb_max, nks_min, lds, s)                          \
+                       : launch_ks_rb<MM, 8, false>(bt, rb_max, nks_min, lds, s);                        \
+    case 4: return vec ? launch_ks_rb<MM, 4, true>(bt, rb_max, nks_min, lds, s)                          \
+                       : launch_ks_rb<MM, 4, false>(bt, rb_max, nks_min, lds, s);                        \
+    default: return hipErrorInvalidValue;                                                        \
   }
   switch (M) {
     case 1: AQLM_GEMV_COPIES(1)
