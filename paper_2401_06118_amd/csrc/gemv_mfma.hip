@@ -41,6 +41,7 @@ namespace {
 constexpr int kWaves = 16;
 constexpr int kThreads = kWaves * kWave;
 constexpr int kMaxRB = 8;  // 16-row blocks per workgroup
+constexpr int kInFlight = 3;  // code items a K-slice-major wave loads ahead
 
 template <int B>
 struct GCfg {
@@ -122,12 +123,15 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
   uint4* x_lds = lds + kCbEntries;
   float* part = reinterpret_cast<float*>(x_lds + bt.xg_max);
 
-  // 1. small loads first (codebooks, x): vector-memory loads retire in issue
+  // 1. small loads first (codebooks, x, scales): vector-memory loads retire in issue
   // order, so these complete without waiting for the HBM code stream.
   uint4 cbv = make_uint4(0, 0, 0, 0);
   if constexpr (B == 8) {
     if (tid < M * 256) cbv = cb[tid];
   }
+  // this thread's output row scale, needed only at the end (an unconditional
+  // load of a clamped row, so that nothing waits for it here)
+  const uint16_t sc = bt.p[p].scales[row0 + (tid < rows ? tid : rows - 1)];
   uint4 xv[C::kXL];
 #pragma unroll
   for (int i = 0; i < C::kXL; ++i) {
@@ -263,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
     float s = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) s += part[(rb * kWaves + w) * 16 + rr];
-    bt.p[p].y[row0 + tid] = f2h(h2f(bt.p[p].scales[row0 + tid]) * s);
+    bt.p[p].y[row0 + tid] = f2h(h2f(sc) * s);
   }
 }
 
@@ -271,13 +275,21 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
 // of the workgroup's RB row blocks.  For each of its K-slices it reads the
 // x slices of its four code slots once into registers (column-0 lanes
 // only), then runs the RB items (row blocks) of that slice, each into its own
-// accumulator, so no partial sums move until the end.  Code loads run D
-// K-slices ahead (D * RB items, about four).
+// accumulator, so no partial sums move until the end.  Code loads run
+// kInFlight items ahead through a ring of D K-slices.
 template <int M, int COPIES, int RB, int D, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   using C = GCfg<8>;
   constexpr int kXS = C::kCPL / M;  // x slices per code slot per K-slice
   constexpr int kStep = RB >= 5 ? 2 : 4;  // codewords gathered per block before their MFMAs
+  // The wave's items run K-slice major, (j, rb) -> item j * RB + rb, through a
+  // ring of kSlots code registers (D K-slices of RB blocks).  Only kInFlight
+  // items are loaded ahead: each consumed item triggers the load of the item
+  // kInFlight places later.  Requesting a whole workgroup's codes at once
+  // would let the memory system finish some workgroups' streams long before
+  // others, whose compute would then run after the stream instead of with it.
+  constexpr int kSlots = D * RB;
+  constexpr int kAhead = kInFlight < kSlots ? kInFlight : kSlots;
   extern __shared__ uint4 lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -304,9 +316,12 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   uint4* x_lds = lds + M * 256 * COPIES;
   float* part = reinterpret_cast<float*>(x_lds + bt.xg_max);
 
-  // 1. codebooks and x first (they retire before the code stream).
+  // 1. codebooks, x and scales first (they retire before the code stream).
   uint4 cbv = make_uint4(0, 0, 0, 0);
   if (tid < M * 256) cbv = cb[tid];
+  // this thread's output row scale, needed only at the end (an unconditional
+  // load of a clamped row, so that nothing waits for it here)
+  const uint16_t sc = bt.p[p].scales[row0 + (tid < rows ? tid : rows - 1)];
   uint4 xv[C::kXL];
 #pragma unroll
   for (int i = 0; i < C::kXL; ++i) {
@@ -315,8 +330,8 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
     if (grp < G) xv[i] = x[grp];
   }
 
-  // 2. code loads for the first D K-slices (rows past the end repeat the last
-  // row; K-slices past the wave's last repeat that slice; never used).
+  // 2. code loads for the first kAhead items (rows past the end repeat the
+  // last row; their sums are never stored).
   const uint32_t slot_off = (uint32_t)slot * 16u;
   int row_off[RB];
 #pragma unroll
@@ -324,20 +339,6 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
     const int row = rb * 16 + r16;
     row_off[rb] = (row < rows ? row : rows - 1) * (int)pitch;
   }
-  auto issue = [&](int j, uint32_t (&w)[RB][4]) {
-    const int jj = j < nks ? j : (nks > 0 ? nks - 1 : 0);
-    const uint32_t off = (uint32_t)(wave + jj * kWaves) * 64u + slot_off;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      if constexpr (VEC) {
-        const uint32_t o = (uint32_t)row_off[rb] + (off < pitch ? off : 0u);
-        const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
-        w[rb][0] = v[0]; w[rb][1] = v[1]; w[rb][2] = v[2]; w[rb][3] = v[3];
-      } else {
-        load_codes_bytes<8>(wg_codes + row_off[rb], pitch, off, w[rb]);
-      }
-    }
-  };
   auto issue_rb = [&](int j, int rb, uint32_t (&w)[4]) {
     const int jj = j < nks ? j : (nks > 0 ? nks - 1 : 0);
     const uint32_t off = (uint32_t)(wave + jj * kWaves) * 64u + slot_off;
@@ -351,7 +352,8 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   };
   uint32_t ring[D][RB][4];
 #pragma unroll
-  for (int d = 0; d < D; ++d) issue(d, ring[d]);
+  for (int i = 0; i < kAhead; ++i)
+    if (i / RB < nks) issue_rb(i / RB, i % RB, ring[i / RB][i % RB]);
 
   // 3. stage codebook copies, x and zeroed partials.
   if (tid < M * 256) {
@@ -372,76 +374,82 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   uint32_t base_m[M];
 #pragma unroll
   for (int m = 0; m < M; ++m) base_m[m] = cb_base + ((uint32_t)m << 16) + copy_off;
-  f4_t acc[RB];
+  {
+    f4_t acc[RB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) acc[rb] = f4_t{0.f, 0.f, 0.f, 0.f};
-  f4_t acc_odd = {0.f, 0.f, 0.f, 0.f};  // second chain of an unpaired last block
-  uint4 xr[kXS];
+    for (int rb = 0; rb < RB; ++rb) acc[rb] = f4_t{0.f, 0.f, 0.f, 0.f};
+    f4_t acc_odd = {0.f, 0.f, 0.f, 0.f};  // second chain of an unpaired last block
+    uint4 xr[kXS];
 #pragma unroll
-  for (int s2 = 0; s2 < kXS; ++s2) xr[s2] = make_uint4(0, 0, 0, 0);
+    for (int s2 = 0; s2 < kXS; ++s2) xr[s2] = make_uint4(0, 0, 0, 0);
 
-  const int rb_live = (rows + 15) / 16;  // row blocks this workgroup really has (<= RB)
-  for (int j0 = 0; j0 < nks; j0 += D) {
+    for (int j0 = 0; j0 < nks; j0 += D) {
 #pragma unroll
-    for (int d = 0; d < D; ++d) {
-      const int j = j0 + d;
-      if (j < nks) {
-        const int ks = wave + j * kWaves;
-        if (r16 == 0) {
-          const uint4* xs = x_lds + (((uint32_t)ks * C::kKS + (uint32_t)slot * C::kCPL) / M);
+      for (int d = 0; d < D; ++d) {
+        const int j = j0 + d;
+        if (j < nks) {
+          const int ks = wave + j * kWaves;
+          if (r16 == 0) {
+            const uint4* xs = x_lds + (((uint32_t)ks * C::kKS + (uint32_t)slot * C::kCPL) / M);
 #pragma unroll
-          for (int s2 = 0; s2 < kXS; ++s2) xr[s2] = xs[s2];
+            for (int s2 = 0; s2 < kXS; ++s2) xr[s2] = xs[s2];
+          }
         }
-      }
-      // Row blocks two at a time, their MFMAs interleaved so that two
-      // accumulation chains are in flight; a lone block alternates two
-      // accumulators.  Each block's codes are reloaded for K-slice j + D as
-      // soon as they are consumed.
+        // Row blocks two at a time, their MFMAs interleaved so that two
+        // accumulation chains are in flight (a lone block alternates two
+        // accumulators).  Blocks past the workgroup's last row read the codes
+        // of its last row (their sums are never stored), so the loop has no
+        // data-dependent branches.  Consuming an item starts the load of the
+        // item kAhead places later, if the wave has it.
+        const bool live = j < nks;
 #pragma unroll
-      for (int rb = 0; rb < RB; rb += 2) {
-        const bool pair = rb + 1 < RB;
-        const bool live = j < nks && rb < rb_live;
-        const bool live2 = pair && j < nks && rb + 1 < rb_live;
-        if (live) {
+        for (int rb = 0; rb < RB; rb += 2) {
+          const bool pair = rb + 1 < RB;
+          if (live) {
 #pragma unroll
-          for (int t0 = 0; t0 < C::kCPL; t0 += kStep) {
-            uint4 av[kStep], bv[kStep];
+            for (int t0 = 0; t0 < C::kCPL; t0 += kStep) {
+              uint4 av[kStep], bv[kStep];
 #pragma unroll
-            for (int u = 0; u < kStep; ++u) {
-              const int t = t0 + u;
-              av[u] = lds_load16(
-                  cw_addr<M, COPIES>(ring[d][rb][t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M));
-              if (pair)
-                bv[u] = lds_load16(
-                    cw_addr<M, COPIES>(ring[d][pair ? rb + 1 : rb][t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M));
-            }
+              for (int u = 0; u < kStep; ++u) {
+                const int t = t0 + u;
+                av[u] = lds_load16(
+                    cw_addr<M, COPIES>(ring[d][rb][t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M));
+                if (pair)
+                  bv[u] = lds_load16(cw_addr<M, COPIES>(ring[d][pair ? rb + 1 : rb][t / 4], t % 4, base_m[t % M],
+                                                        copy_off + cb_base, t % M));
+              }
 #pragma unroll
-            for (int u = 0; u < kStep; ++u) {
-              const int t = t0 + u;
-              const h8_t xh = __builtin_bit_cast(h8_t, xr[t / M]);
-              if (pair) {
-                acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, acc[rb], 0, 0, 0);
-                if (live2)
+              for (int u = 0; u < kStep; ++u) {
+                const int t = t0 + u;
+                const h8_t xh = __builtin_bit_cast(h8_t, xr[t / M]);
+                if (pair) {
+                  acc[rb] =
+                      __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, acc[rb], 0, 0, 0);
                   acc[pair ? rb + 1 : rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
                       __builtin_bit_cast(h8_t, bv[u]), xh, acc[pair ? rb + 1 : rb], 0, 0, 0);
-              } else {
-                f4_t& a = (u % 2 == 0) ? acc[rb] : acc_odd;
-                a = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, a, 0, 0, 0);
+                } else {
+                  f4_t& a = (u % 2 == 0) ? acc[rb] : acc_odd;
+                  a = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, a, 0, 0, 0);
+                }
               }
             }
           }
+#pragma unroll
+          for (int q = 0; q < (pair ? 2 : 1); ++q) {
+            const int target = d * RB + rb + q + kAhead;  // item position relative to K-slice j0
+            const int jt = j0 + target / RB;
+            if (jt < nks) issue_rb(jt, target % RB, ring[(target % kSlots) / RB][target % RB]);
+          }
         }
-        issue_rb(j + D, rb, ring[d][rb]);
-        if (pair) issue_rb(j + D, rb + 1, ring[d][pair ? rb + 1 : rb]);
       }
     }
-  }
-  if constexpr (RB % 2 == 1) acc[RB - 1] += acc_odd;
-  if (r16 == 0) {
+    if constexpr (RB % 2 == 1) acc[RB - 1] += acc_odd;
+    if (r16 == 0) {
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) part[(rb * kWaves + wave) * 16 + 4 * slot + e] = acc[rb][e];
+        for (int e = 0; e < 4; ++e) part[(rb * kWaves + wave) * 16 + 4 * slot + e] = acc[rb][e];
+    }
   }
   __syncthreads();
 
@@ -451,7 +459,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
     float s = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) s += part[(rb * kWaves + w) * 16 + rr];
-    bt.p[p].y[row0 + tid] = f2h(h2f(bt.p[p].scales[row0 + tid]) * s);
+    bt.p[p].y[row0 + tid] = f2h(h2f(sc) * s);
   }
 }
 
