@@ -354,7 +354,7 @@ def main():
     avg_launch_ms = ms / len(launches)
     bytes_per_launch = step_bytes / len(launches)
     achieved = bytes_per_launch / (avg_launch_ms * 1e6)
-    digest = source_digest("gemv_mfma.hip", "common.h")
+    digest = source_digest("gemv_mfma.hip", "stream_common.h", "common.h")
     kname = kernel_name(M, B)
     traffic = measured_traffic(f"{kname}:{args.workload}", digest)
 

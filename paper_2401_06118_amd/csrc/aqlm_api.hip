@@ -96,6 +96,9 @@ int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const ui
   if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (n == 1) return status_of(gemv_dispatch(L, x, y, s));
+  // 2..16 tokens with M = 2 or 4 8-bit codebooks: the matrix-vector kernel's
+  // scheme with one MFMA column per token; otherwise the tiled kernel.
+  if (aqlm::gemm_nb_supported(L, (int32_t)n)) return status_of(aqlm::launch_gemm_nb(L, (int32_t)n, x, y, s));
   if (aqlm::mfma_supported(L)) return status_of(aqlm::launch_gemm_mfma(L, (int32_t)n, x, y, s));
   // Formats the matrix-core kernel does not tile (M = 3, 5, 6, 7): one
   // matrix-vector launch per activation row.

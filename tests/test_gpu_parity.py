@@ -199,6 +199,29 @@ def test_prefill_layer_sampled_rows(n, M, B):
     check_products(lay, y, rows)
 
 
+@pytest.mark.parametrize("d_out,d_in,M,n", [
+    (1000, 4096, 2, 2), (1000, 4096, 2, 16), (1000, 4096, 4, 5), (1000, 4096, 4, 16),
+    (300, 11008, 4, 3), (300, 11008, 4, 16), (300, 11008, 2, 16), (4100, 2048, 4, 7),
+    (17, 264, 4, 9), (16, 4096, 2, 4),
+])
+def test_gemm_small_batch_shapes(d_out, d_in, M, n):
+    """2..16 tokens over several K-slice rounds, ragged rows, aligned and
+    unaligned code pitches, and the LDS budgets of n = 16."""
+    print(f"[gemm-nb] {d_out}x{d_in} M={M} n={n}", flush=True)
+    lay = synth.layer(5500 + d_out + d_in + M + n, d_out, d_in, M, 8, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemm_small_batch(codes, cb, sc, x)
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y))
+
+
+def test_gemm_small_batch_deterministic():
+    lay = synth.layer(14, 3000, 4096, 4, 8, n=8)
+    codes, cb, sc, x = to_device(lay)
+    ys = [aq().gemm_small_batch(codes, cb, sc, x).cpu().numpy().view(np.uint16) for _ in range(3)]
+    assert all(np.array_equal(ys[0], v) for v in ys[1:])
+
+
 def test_gemm_deterministic():
     lay = synth.layer(12, 2048, 2048, 2, 8, n=37)
     codes, cb, sc, x = to_device(lay)
