@@ -54,6 +54,9 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
 
 int status_of(hipError_t e) { return e == hipSuccess ? AQLM_OK : AQLM_ERR_HIP; }
 
+// Above this many tokens the dequantize-then-multiply prefill kernel is used.
+constexpr int64_t kSmallBatchMax = 16;
+
 // n = 1: the matrix-core kernel for M in {1, 2, 4} (B = 8) and 1x16; the
 // vector-ALU kernel for the other codebook counts.
 hipError_t gemv_dispatch(const aqlm::Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s) {
@@ -99,6 +102,8 @@ int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const ui
   // 2..16 tokens with M = 2 or 4 8-bit codebooks: the matrix-vector kernel's
   // scheme with one MFMA column per token; otherwise the tiled kernel.
   if (aqlm::gemm_nb_supported(L, (int32_t)n)) return status_of(aqlm::launch_gemm_nb(L, (int32_t)n, x, y, s));
+  // More tokens: dequantized weight tiles feed a dense MFMA product.
+  if (n > kSmallBatchMax && aqlm::prefill_supported(L)) return status_of(aqlm::launch_prefill(L, (int32_t)n, x, y, s));
   if (aqlm::mfma_supported(L)) return status_of(aqlm::launch_gemm_mfma(L, (int32_t)n, x, y, s));
   // Formats the matrix-core kernel does not tile (M = 3, 5, 6, 7): one
   // matrix-vector launch per activation row.

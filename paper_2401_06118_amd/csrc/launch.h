@@ -51,6 +51,8 @@ hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream
 hipError_t launch_gemm_mfma(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
 bool mfma_supported(const Layer& L);
 bool gemm_nb_supported(const Layer& L, int32_t n);
+bool prefill_supported(const Layer& L);
+hipError_t launch_prefill(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
 hipError_t launch_gemm_nb(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
 
 int num_cus();

@@ -215,6 +215,29 @@ def test_gemm_small_batch_shapes(d_out, d_in, M, n):
     check_products(lay, fp16_to_np(y))
 
 
+@pytest.mark.parametrize("d_out,d_in,M,B,n", [
+    (300, 1040, 2, 8, 17), (300, 1040, 4, 8, 300), (129, 520, 1, 8, 40), (1000, 4096, 2, 8, 256),
+    (1000, 4096, 4, 8, 513), (260, 4104, 1, 16, 100), (128, 64, 4, 8, 257), (4096, 512, 2, 8, 1024),
+    (7, 2056, 1, 16, 33),
+])
+def test_prefill_shapes(d_out, d_in, M, B, n):
+    """Many tokens: ragged row and token tiles, K not a multiple of the
+    64-input step, aligned and unaligned code pitches, every format."""
+    print(f"[prefill-shapes] {d_out}x{d_in} M={M} B={B} n={n}", flush=True)
+    lay = synth.layer(5800 + d_out + d_in + M + B + n, d_out, d_in, M, B, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemm_small_batch(codes, cb, sc, x)
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y))
+
+
+def test_prefill_deterministic():
+    lay = synth.layer(15, 700, 2048, 4, 8, n=300)
+    codes, cb, sc, x = to_device(lay)
+    ys = [aq().gemm_small_batch(codes, cb, sc, x).cpu().numpy().view(np.uint16) for _ in range(3)]
+    assert all(np.array_equal(ys[0], v) for v in ys[1:])
+
+
 def test_gemm_small_batch_deterministic():
     lay = synth.layer(14, 3000, 4096, 4, 8, n=8)
     codes, cb, sc, x = to_device(lay)
