@@ -62,6 +62,9 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
+    ap.add_argument("--batch-case", metavar="M,B,n", action="append",
+                    help="only time the 11008x4096 product of this format and token count "
+                         "(repeatable) and print its row")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy a few times (the reference kernel for "
                          "scaling HBM byte counters) and exit")
@@ -270,12 +273,15 @@ def single_layer_rows(aq, torch):
     return rows
 
 
-def batch_rows(aq, torch):
+def batch_rows(aq, torch, cases=None):
     """11008x4096 1x16 and 4x8 with n activation rows (the small-batch and
-    prefill path), plus dequantization of the same layers."""
+    prefill path), plus dequantization of the same layers.  ``cases``, a list
+    of (M, B, n), restricts the run to those products (no dequantization)."""
     rows = []
     for M, B in ((1, 16), (4, 8)):
         for n in (1, 4, 16, 256, 2048):
+            if cases is not None and (M, B, n) not in cases:
+                continue
             from paper_2401_06118_amd import format as fmt
             shp = fmt.AqlmShape(11008, 4096, M, B)
             reps = 1 if n >= 256 else max(2, (1 << 30) // shp.codes_bytes() + 1)
@@ -289,6 +295,8 @@ def batch_rows(aq, torch):
                          "mfma_frac": shp.flops(n) / (ms * 1e9) / MFMA_F16_PEAK_TFS})
             del layers
             torch.cuda.empty_cache()
+        if cases is not None:
+            continue
         L = DeviceLayer(700000 + M, 11008, 4096, M, B)
         w = torch.empty((11008, 4096), dtype=torch.float16, device="cuda")
         ms = time_steps(lambda: aq.dequantize(L.codes, L.codebooks, L.scales, out=w), steps=10, warmup=3)
@@ -334,6 +342,13 @@ def main():
         copy_calibration()
         return
     import torch
+    if args.batch_case:
+        import paper_2401_06118_amd as aq
+        from paper_2401_06118_amd import _lib
+        _lib.load()
+        cases = [tuple(int(v) for v in c.split(",")) for c in args.batch_case]
+        print(json.dumps({"batch": batch_rows(aq, torch, cases)}), flush=True)
+        return
 
     import paper_2401_06118_amd as aq
     from paper_2401_06118_amd import _lib
