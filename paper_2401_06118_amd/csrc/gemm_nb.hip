@@ -61,7 +61,11 @@ __global__ __launch_bounds__(kThreadsNB) void k_gemm_nb(const GemmNbArgs a) {
   constexpr int kXG = N::kXG;
   constexpr int kStep = RB >= 5 ? 2 : 4;
   constexpr int kSlots = D * RB;
-  constexpr int kAhead = kInFlightNB < kSlots ? kInFlightNB : kSlots;
+  // both items of a row-block pair must be in flight when the pair starts
+  constexpr int kAheadMin = RB >= 2 ? 2 : 1;
+  constexpr int kAheadWant = kInFlightNB > kAheadMin ? kInFlightNB : kAheadMin;
+  constexpr int kAhead = kAheadWant < kSlots ? kAheadWant : kSlots;
+  static_assert(kAhead >= kAheadMin, "a pair of row blocks needs both items loaded");
   extern __shared__ uint4 lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);

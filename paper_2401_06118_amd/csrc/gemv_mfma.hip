@@ -245,7 +245,12 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   // would let the memory system finish some workgroups' streams long before
   // others, whose compute would then run after the stream instead of with it.
   constexpr int kSlots = D * RB;
-  constexpr int kAhead = kInFlight < kSlots ? kInFlight : kSlots;
+  // Row blocks are consumed two at a time, so both items of a pair must be in
+  // flight when the pair starts: at least two items ahead when RB >= 2.
+  constexpr int kAheadMin = RB >= 2 ? 2 : 1;
+  constexpr int kAheadWant = kInFlight > kAheadMin ? kInFlight : kAheadMin;
+  constexpr int kAhead = kAheadWant < kSlots ? kAheadWant : kSlots;
+  static_assert(kAhead >= kAheadMin, "a pair of row blocks needs both items loaded");
   extern __shared__ uint4 lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -311,7 +316,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   for (int i = 0; i < kAhead; ++i)
     if (i / RB < nks) issue_rb(i / RB, i % RB, ring[i / RB][i % RB]);
 
-  // 3. stage codebook copies, x and zeroed partials.
+  // 3. stage codebook copies and x.
   if (tid < M * 256) {
 #pragma unroll
     for (int k = 0; k < COPIES; ++k) cb_lds[tid * COPIES + ((k + lane) % COPIES)] = cbv;
@@ -321,8 +326,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
     const int grp = tid + i * kThreads;
     if (grp < xg) x_lds[grp] = xv[i];
   }
-  for (int e = tid; e < RB * kWaves * 16; e += kThreads) part[e] = 0.f;
-  __syncthreads();
+  __syncthreads();  // (no zeroing of the partials: every wave writes all of its slots)
 
   // 4. K-slices of this wave.
   const uint32_t copy_off = (uint32_t)(lane % COPIES) * 16u;
