@@ -57,10 +57,12 @@ int status_of(hipError_t e) { return e == hipSuccess ? AQLM_OK : AQLM_ERR_HIP; }
 // Above this many tokens the dequantize-then-multiply prefill kernel is used.
 constexpr int64_t kSmallBatchMax = 16;
 
-// n = 1: the matrix-core kernel for M in {1, 2, 4} (B = 8) and 1x16; the
-// vector-ALU kernel for the other codebook counts.
+// n = 1: the matrix-core kernel for M in {1, 2, 4} (B = 8) and 1x16 when x
+// fits in its LDS staging (d_in up to 32768 for 8-bit codes, 65536 for
+// 16-bit); the vector-ALU kernel otherwise.
 hipError_t gemv_dispatch(const aqlm::Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s) {
-  if (aqlm::gemv_mfma_supported(L.M, L.B)) return aqlm::launch_gemv_mfma(&L, &x, &y, 1, s);
+  if (aqlm::gemv_mfma_supported(L.M, L.B) && aqlm::gemv_mfma_fits(&L, 1))
+    return aqlm::launch_gemv_mfma(&L, &x, &y, 1, s);
   return aqlm::launch_gemv(L, x, y, s);
 }
 
@@ -133,7 +135,8 @@ int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t 
   hipStream_t s = static_cast<hipStream_t>(stream);
   bool same_class = true;
   for (int i = 1; i < count; ++i) same_class = same_class && Ls[i].vec_codes == Ls[0].vec_codes;
-  if (aqlm::gemv_mfma_supported(M, B) && same_class) return status_of(aqlm::launch_gemv_mfma(Ls, xs, ys, count, s));
+  if (aqlm::gemv_mfma_supported(M, B) && same_class && aqlm::gemv_mfma_fits(Ls, count))
+    return status_of(aqlm::launch_gemv_mfma(Ls, xs, ys, count, s));
   for (int i = 0; i < count; ++i) {
     const hipError_t e = gemv_dispatch(Ls[i], xs[i], ys[i], s);
     if (e != hipSuccess) return AQLM_ERR_HIP;

@@ -497,6 +497,21 @@ hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStrea
 
 bool gemv_mfma_supported(int M, int B) { return (B == 16 && M == 1) || (B == 8 && (M == 1 || M == 2 || M == 4)); }
 
+// Whether x (staged whole in LDS, at most kXL groups per thread) and the
+// partial sums fit, next to at least one codebook copy for 8-bit codes.
+bool gemv_mfma_fits(const Layer* Ls, int count) {
+  for (int i = 0; i < count; ++i) {
+    const Layer& L = Ls[i];
+    const int kCPL = (L.B == 8) ? 16 : 8, kKS = 4 * kCPL, xl = (L.B == 8) ? 4 : 8;
+    const int64_t KS = ((int64_t)L.G * L.M * (L.B / 8) + 63) / 64;
+    const int64_t xg = KS * (kKS / L.M);
+    if (xg > (int64_t)xl * kThreads) return false;
+    const size_t need = (size_t)xg * 16 + (size_t)kMaxRB * kWaves * 16 * 4 + (L.B == 8 ? (size_t)L.M * 256 * 16 : 0);
+    if (need > 160 * 1024) return false;
+  }
+  return true;
+}
+
 // Deal workgroups to problems, pick rows per workgroup and items per wave,
 // size LDS, and launch.  All problems share (M, B) and the code-pitch
 // alignment class.

@@ -45,6 +45,7 @@ struct GemvBatch {
 
 hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s);
 bool gemv_mfma_supported(int M, int B);
+bool gemv_mfma_fits(const Layer* Ls, int count);
 hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
                             hipStream_t s);
 hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s);

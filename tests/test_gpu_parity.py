@@ -238,6 +238,21 @@ def test_prefill_deterministic():
     assert all(np.array_equal(ys[0], v) for v in ys[1:])
 
 
+@pytest.mark.parametrize("d_out,d_in,M,B", [(24, 40960, 2, 8), (40, 40968, 4, 8), (17, 65544, 1, 16), (8, 131072, 1, 8)])
+def test_gemv_wide_layers(d_out, d_in, M, B):
+    """d_in beyond what the matrix-core kernel stages in LDS: the vector-ALU
+    kernel takes over (also through the grouped entry point)."""
+    print(f"[gemv-wide] {d_out}x{d_in} M={M} B={B}", flush=True)
+    lay = synth.layer(5900 + d_in + M, d_out, d_in, M, B)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemv(codes, cb, sc, x[0])
+    y2 = torch.empty_like(y)
+    aq().gemv_grouped([(codes, cb, sc, x[0], y2)])
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y)[None])
+    check_products(lay, fp16_to_np(y2)[None])
+
+
 def test_gemm_small_batch_deterministic():
     lay = synth.layer(14, 3000, 4096, 4, 8, n=8)
     codes, cb, sc, x = to_device(lay)
