@@ -14,6 +14,14 @@ namespace aqlm {
 
 constexpr int kWave = 64;
 
+// A compile-time integer passed as an argument, so that one lambda can be
+// instantiated per value (register sets and unrolled schedules chosen at
+// compile time).
+template <int V>
+struct IntC {
+  static constexpr int value = V;
+};
+
 __device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
 // Round to fp16 with the hardware conversion (round to nearest even under the
 // default MODE; fp16 subnormals are kept).

@@ -42,7 +42,6 @@ namespace {
 constexpr int kWaves = 16;
 constexpr int kThreads = kWaves * kWave;
 constexpr int kMaxRB = 8;  // 16-row blocks per workgroup
-constexpr int kInFlight = 3;  // code items a K-slice-major wave loads ahead
 
 template <int M, int B, int COPIES, int PF, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
@@ -232,25 +231,27 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
 // x slices of its four code slots once into registers (column-0 lanes
 // only), then runs the RB items (row blocks) of that slice, each into its own
 // accumulator, so no partial sums move until the end.  Code loads run
-// kInFlight items ahead through a ring of D K-slices.
+// through a ring of D K-slices, all of its items in flight.
 template <int M, int COPIES, int RB, int D, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   using C = GCfg<8>;
   constexpr int kXS = C::kCPL / M;  // x slices per code slot per K-slice
   constexpr int kStep = RB >= 5 ? 2 : 4;  // codewords gathered per block before their MFMAs
   // The wave's items run K-slice major, (j, rb) -> item j * RB + rb, through a
-  // ring of kSlots code registers (D K-slices of RB blocks).  Only kInFlight
-  // items are loaded ahead: each consumed item triggers the load of the item
-  // kInFlight places later.  Requesting a whole workgroup's codes at once
-  // would let the memory system finish some workgroups' streams long before
-  // others, whose compute would then run after the stream instead of with it.
+  // ring of kSlots code registers (D K-slices of RB blocks).  Consuming an
+  // item starts the load of the item kAhead places later (kAhead <= kSlots,
+  // so its slot is free), so kAhead items are in flight.  Row blocks are
+  // consumed in pairs, so a load is used at least kAhead - 2 items after it
+  // is requested.
   constexpr int kSlots = D * RB;
-  // Row blocks are consumed two at a time, so both items of a pair must be in
-  // flight when the pair starts: at least two items ahead when RB >= 2.
-  constexpr int kAheadMin = RB >= 2 ? 2 : 1;
-  constexpr int kAheadWant = kInFlight > kAheadMin ? kInFlight : kAheadMin;
+  // Paired blocks: four items ahead, so each load has a whole pair of items
+  // computed between its request and its use.  Measured on the Llama-2
+  // shapes, five or six ahead were slower (more of a workgroup's stream in
+  // flight at once delays the items that every wave needs first).  Single
+  // blocks: the whole ring.
+  constexpr int kAheadWant = RB >= 2 ? 4 : 8;
   constexpr int kAhead = kAheadWant < kSlots ? kAheadWant : kSlots;
-  static_assert(kAhead >= kAheadMin, "a pair of row blocks needs both items loaded");
+  static_assert(RB < 2 || kAhead >= 2, "both items of a pair must be requested before the pair starts");
   extern __shared__ uint4 lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -313,8 +314,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   };
   uint32_t ring[D][RB][4];
 #pragma unroll
-  for (int i = 0; i < kAhead; ++i)
-    if (i / RB < nks) issue_rb(i / RB, i % RB, ring[i / RB][i % RB]);
+  for (int i = 0; i < kAhead; ++i) issue_rb(i / RB, i % RB, ring[i / RB][i % RB]);
 
   // 3. stage codebook copies and x.
   if (tid < M * 256) {
@@ -343,11 +343,19 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
 #pragma unroll
     for (int s2 = 0; s2 < kXS; ++s2) xr[s2] = make_uint4(0, 0, 0, 0);
 
-    for (int j0 = 0; j0 < nks; j0 += D) {
+    // One ring period: D K-slices starting at j0.  Consuming an item loads
+    // the item kAhead places later.  ISSUE: 2 = every such item exists (the
+    // main loop), 1 = load it if it exists, 0 = the last period (only items
+    // inside this period remain).  In the main loop every load is
+    // unconditional, so the wait before each use counts exactly the loads
+    // issued after it.
+    auto period = [&](int j0, auto issue) {
+      constexpr int kIssue = decltype(issue)::value;
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         const int j = j0 + d;
-        if (j < nks) {
+        const bool live = j < nks;
+        if (live) {
           const int ks = wave + j * kWaves;
           if (r16 == 0) {
             const uint4* xs = x_lds + (((uint32_t)ks * C::kKS + (uint32_t)slot * C::kCPL) / M);
@@ -359,9 +367,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
         // accumulation chains are in flight (a lone block alternates two
         // accumulators).  Blocks past the workgroup's last row read the codes
         // of its last row (their sums are never stored), so the loop has no
-        // data-dependent branches.  Consuming an item starts the load of the
-        // item kAhead places later, if the wave has it.
-        const bool live = j < nks;
+        // data-dependent branches.
 #pragma unroll
         for (int rb = 0; rb < RB; rb += 2) {
           const bool pair = rb + 1 < RB;
@@ -398,11 +404,26 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
           for (int q = 0; q < (pair ? 2 : 1); ++q) {
             const int target = d * RB + rb + q + kAhead;  // item position relative to K-slice j0
             const int jt = j0 + target / RB;
-            if (jt < nks) issue_rb(jt, target % RB, ring[(target % kSlots) / RB][target % RB]);
+            // (target is a compile-time constant here, so only ISSUE == 1
+            // leaves a run-time test; a target inside the last period is
+            // loaded even if past the wave's end: issue_rb repeats the last
+            // K-slice.)
+            if (kIssue == 2 || (kIssue == 1 && jt < nks) || (kIssue == 0 && target < kSlots))
+              issue_rb(jt, target % RB, ring[(target % kSlots) / RB][target % RB]);
           }
+          // Keep the loads here: the scheduler would otherwise sink them
+          // towards their use, leaving the HBM latency exposed.
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
+    };
+    int j0 = 0;
+    for (; j0 + 2 * D <= nks; j0 += D) period(j0, IntC<2>{});
+    if (j0 + D < nks) {
+      period(j0, IntC<1>{});
+      j0 += D;
     }
+    if (j0 < nks) period(j0, IntC<0>{});
     if constexpr (RB % 2 == 1) acc[RB - 1] += acc_odd;
     if (r16 == 0) {
 #pragma unroll
@@ -441,14 +462,24 @@ hipError_t launch_ks(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
 // spilling (1024 threads: 128 VGPRs per lane); M = 1 holds 16 x slices.
 constexpr int ks_rb_cap(int M) { return M == 1 ? 2 : 7; }
 
-// Code-load lookahead in K-slices: about four items, but never more
-// K-slices than a wave owns (extra loads would only repeat its last one).
+// Ring depth in K-slices: up to about eight items in flight per wave, within
+// the register budget, and no more K-slices than a wave owns (extra slots
+// would only repeat its last one).  Paired row blocks need at least four
+// slots.
 template <int M, int COPIES, int RB, bool VEC>
 hipError_t launch_ks_d(const GemvBatch& bt, int nks, size_t lds_bytes, hipStream_t s) {
-  constexpr int D4 = RB >= 4 ? 1 : (RB == 1 ? 4 : 2);
-  if (D4 >= 4 && nks >= 4) return launch_ks<M, COPIES, RB, (D4 >= 4 ? 4 : 1), VEC>(bt, lds_bytes, s);
-  if (D4 >= 2 && nks >= 2) return launch_ks<M, COPIES, RB, (D4 >= 2 ? 2 : 1), VEC>(bt, lds_bytes, s);
-  return launch_ks<M, COPIES, RB, 1, VEC>(bt, lds_bytes, s);
+  constexpr int kDMax = RB >= 5 ? 1 : (RB >= 3 ? 2 : (RB == 2 ? 4 : 8));
+  constexpr int kDMin = (RB == 2 || RB == 3) ? 2 : 1;
+  if constexpr (kDMax >= 8) {
+    if (nks >= 8) return launch_ks<M, COPIES, RB, 8, VEC>(bt, lds_bytes, s);
+  }
+  if constexpr (kDMax >= 4) {
+    if (nks >= 4) return launch_ks<M, COPIES, RB, 4, VEC>(bt, lds_bytes, s);
+  }
+  if constexpr (kDMax >= 2) {
+    if (nks >= 2 || kDMin == 2) return launch_ks<M, COPIES, RB, 2, VEC>(bt, lds_bytes, s);
+  }
+  return launch_ks<M, COPIES, RB, kDMin, VEC>(bt, lds_bytes, s);
 }
 
 template <int M, int COPIES, bool VEC>

@@ -58,11 +58,6 @@ struct PfCfg {
   static constexpr size_t kLds = kCbBytes + 2 * (size_t)(kATileU4 + kXTileU4) * 16;
 };
 
-template <int V>
-struct IntC {
-  static constexpr int value = V;
-};
-
 template <int B>
 __device__ __forceinline__ uint32_t code_at(const uint32_t* w, int q) {
   if constexpr (B == 16) return (w[q / 2] >> (16 * (q % 2))) & 0xFFFFu;
