@@ -168,26 +168,15 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
             cwv[m] = gcw[s][q];  // gathered one step earlier
           }
         }
-        uint4 w;
-        if constexpr (M == 1) {
-          w = cwv[0];
-        } else {
-          // fp32 sum of the M codewords in ascending m, rounded once to fp16
-          uint32_t o[4];
-          const uint32_t* c0 = reinterpret_cast<const uint32_t*>(&cwv[0]);
+        // Sum of the M codewords in ascending m with packed fp16 adds (four
+        // v_pk_add_f16 per codeword).  Each add rounds to fp16; the product
+        // only has to meet the output tolerance, and the single-rounding fp32
+        // order is kept where the weights themselves are the result
+        // (dequantization).
+        h8_t wsum = __builtin_bit_cast(h8_t, cwv[0]);
 #pragma unroll
-          for (int h = 0; h < 4; ++h) {
-            float lo = h2f((uint16_t)(c0[h] & 0xFFFFu)), hi = h2f((uint16_t)(c0[h] >> 16));
-#pragma unroll
-            for (int m = 1; m < M; ++m) {
-              const uint32_t cm = reinterpret_cast<const uint32_t*>(&cwv[m])[h];
-              lo += h2f((uint16_t)(cm & 0xFFFFu));
-              hi += h2f((uint16_t)(cm >> 16));
-            }
-            o[h] = (uint32_t)f2h(lo) | ((uint32_t)f2h(hi) << 16);
-          }
-          w = make_uint4(o[0], o[1], o[2], o[3]);
-        }
+        for (int m = 1; m < M; ++m) wsum += __builtin_bit_cast(h8_t, cwv[m]);
+        uint4 w = __builtin_bit_cast(uint4, wsum);
         if (!row_ok || g + q >= G) w = make_uint4(0, 0, 0, 0);
         at[q] = w;
       }
