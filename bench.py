@@ -62,9 +62,10 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
-    ap.add_argument("--batch-case", metavar="M,B,n", action="append",
+    ap.add_argument("--batch-case", metavar="M,B,n[,1]", action="append",
                     help="only time the 11008x4096 product of this format and token count "
-                         "(repeatable) and print its row")
+                         "(repeatable) and print its row; a fourth field 1 times the workspace "
+                         "product (aqlm_gemm) instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy a few times (the reference kernel for "
                          "scaling HBM byte counters) and exit")
@@ -90,6 +91,9 @@ class DeviceLayer:
 
     def gemm(self, aq):
         aq.gemm_small_batch(self.codes, self.codebooks, self.scales, self.x, out=self.y)
+
+    def gemm_ws(self, aq, ws):
+        aq.gemm(self.codes, self.codebooks, self.scales, self.x, workspace=ws, out=self.y)
 
 
 def decode_step_layers(model: str, M: int, B: int, seed0: int):
@@ -280,21 +284,34 @@ def batch_rows(aq, torch, cases=None):
     rows = []
     for M, B in ((1, 16), (4, 8)):
         for n in (1, 4, 16, 256, 2048):
-            if cases is not None and (M, B, n) not in cases:
-                continue
             from paper_2401_06118_amd import format as fmt
             shp = fmt.AqlmShape(11008, 4096, M, B)
-            reps = 1 if n >= 256 else max(2, (1 << 30) // shp.codes_bytes() + 1)
-            layers = [DeviceLayer(800000 + 7 * i + n, 11008, 4096, M, B, n=n) for i in range(reps)]
-            g = graph_of([lambda L=L: L.gemm(aq) for L in layers])
-            ms = time_steps(g.replay, steps=max(3, 8 // reps), warmup=1) / reps
-            del g
-            b = shp.gemv_bytes(n)
-            rows.append({"layer": f"11008x4096 {M}x{B // 8 * 8 if B == 8 else 16}", "n": n, "us": ms * 1e3,
-                         "GBs": b / (ms * 1e6), "TFLOPs": shp.flops(n) / (ms * 1e9),
-                         "mfma_frac": shp.flops(n) / (ms * 1e9) / MFMA_F16_PEAK_TFS})
-            del layers
-            torch.cuda.empty_cache()
+            name = f"11008x4096 {M}x{B // 8 * 8 if B == 8 else 16}"
+            if cases is None or (M, B, n) in cases:
+                reps = 1 if n >= 256 else max(2, (1 << 30) // shp.codes_bytes() + 1)
+                layers = [DeviceLayer(800000 + 7 * i + n, 11008, 4096, M, B, n=n) for i in range(reps)]
+                g = graph_of([lambda L=L: L.gemm(aq) for L in layers])
+                ms = time_steps(g.replay, steps=max(3, 8 // reps), warmup=1) / reps
+                del g
+                b = shp.gemv_bytes(n)
+                rows.append({"layer": name, "n": n, "us": ms * 1e3,
+                             "GBs": b / (ms * 1e6), "TFLOPs": shp.flops(n) / (ms * 1e9),
+                             "mfma_frac": shp.flops(n) / (ms * 1e9) / MFMA_F16_PEAK_TFS})
+                del layers
+                torch.cuda.empty_cache()
+            # the workspace path (aqlm_gemm: dequantize once, dense fp16 product)
+            if n >= 256 and (cases is None or (M, B, n, 1) in cases):
+                L = DeviceLayer(800000 + n, 11008, 4096, M, B, n=n)
+                need = aq.gemm_workspace_bytes(L.codes, L.codebooks, L.scales, n)
+                ws = torch.empty((need,), dtype=torch.uint8, device="cuda")
+                g = graph_of([lambda: L.gemm_ws(aq, ws)])
+                ms = time_steps(g.replay, steps=8, warmup=1)
+                del g
+                rows.append({"layer": name, "n": n, "op": "gemm with workspace", "us": ms * 1e3,
+                             "TFLOPs": shp.flops(n) / (ms * 1e9),
+                             "mfma_frac": shp.flops(n) / (ms * 1e9) / MFMA_F16_PEAK_TFS})
+                del L, ws
+                torch.cuda.empty_cache()
         if cases is not None:
             continue
         L = DeviceLayer(700000 + M, 11008, 4096, M, B)

@@ -46,6 +46,7 @@
 #ifndef AQLM_MI355X_H
 #define AQLM_MI355X_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -58,7 +59,8 @@ enum aqlm_status {
   AQLM_ERR_SHAPE = 2,       /* non-positive or too large size, or d_in % g != 0 */
   AQLM_ERR_UNSUPPORTED = 3, /* (M, B, g) outside the supported set */
   AQLM_ERR_ALIGN = 4,       /* a pointer breaks the alignment rule above */
-  AQLM_ERR_HIP = 5          /* the HIP runtime reported an error */
+  AQLM_ERR_HIP = 5,         /* the HIP runtime reported an error */
+  AQLM_ERR_WORKSPACE = 6    /* aqlm_gemm: workspace smaller than aqlm_gemm_workspace_bytes */
 };
 
 /* Dequantize: w_out[i][j*g + k] = fp16(fp32(sum_m C_m[b[i][j][m]][k]) * s_i)
@@ -107,13 +109,40 @@ int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t 
                       void* stream);
 
 /* Product with n activation rows: y[t][i] = fp16(s_i * sum_c W[i][c] x[t][c])
- * with W reconstructed as above, fp32 accumulation, any n >= 1.  n = 1 runs
- * the matrix-vector kernel; larger n runs a matrix-core (MFMA) kernel that
- * rebuilds each weight fragment once per tile of up to 64 rows of x.
+ * with W reconstructed as above, fp32 accumulation, any n >= 1 (the batched
+ * and prefill products of a layer; the paper times the single-row case,
+ * Sec. 4.3).  n = 1 runs the matrix-vector kernel; 2..16 rows put the rows in
+ * the matrix-core (MFMA) columns of the same scheme; more rows dequantize
+ * weight tiles into on-chip memory once per tile of 128 or 256 rows of x and
+ * feed them to dense fp16 MFMA products.  Needs no workspace.  Results are
+ * within fp32-accumulation accuracy of fp16(W) x, not bit-exact with it.
  * Deterministic. */
 int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
                           int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n,
                           const uint16_t* x, uint16_t* y, void* stream);
+
+/* Device workspace, in bytes, that aqlm_gemm needs for these sizes: d_out *
+ * d_in * 2 (the dequantized weights) when it takes the two-pass path
+ * (n >= 64 and d_in a multiple of 64), else 0.  Returns 0 for invalid sizes
+ * (aqlm_gemm then reports the error). */
+size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n);
+
+/* The product of aqlm_gemm_small_batch with a caller-provided workspace:
+ * for many activation rows the weights are dequantized once into `workspace`
+ * exactly as aqlm_dequantize writes them (scales included, Eq. 2), then a
+ * dense fp16 MFMA product y[t][i] = fp16(sum_c W[i][c] x[t][c]) with fp32
+ * accumulation reads them; this removes the per-tile rebuilding of the
+ * weights that aqlm_gemm_small_batch pays.  `workspace` is DEVICE memory of
+ * at least aqlm_gemm_workspace_bytes(...) bytes, 16-byte aligned, owned by
+ * the caller; its contents are overwritten (they hold W afterwards) and it
+ * must not alias any other argument.  When the size query returns 0 the
+ * workspace is not used and may be NULL, and the call computes exactly what
+ * aqlm_gemm_small_batch computes.  Errors as above, plus AQLM_ERR_NULL for a
+ * needed NULL workspace and AQLM_ERR_WORKSPACE for a small one.
+ * Deterministic. */
+int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+              int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n,
+              const uint16_t* x, uint16_t* y, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static text for a status code (never NULL). */
 const char* aqlm_status_string(int status);

@@ -8,7 +8,9 @@ Eq. 2 and Fig. 3).  This package exposes the three operations of the C ABI in
 - :func:`dequantize` - rebuild the fp16 weight matrix, bit-exact;
 - :func:`gemv` - the token-generation matrix-vector product (Sec. 4.3);
 - :func:`gemv_grouped` - several independent matrix-vector products in one launch;
-- :func:`gemm_small_batch` - the same product for n activation rows.
+- :func:`gemm_small_batch` - the same product for n activation rows;
+- :func:`gemm` - that product with a workspace: for many rows the weights are
+  dequantized once, then a dense fp16 matrix-core product reads them.
 
 Every computation runs in the hand-written HIP kernels of
 ``libaqlm_mi355x.so``; this module only marshals arguments.
@@ -24,7 +26,8 @@ import torch
 from . import _lib
 from ._lib import AqlmError, status_string  # noqa: F401
 
-__all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "AqlmError", "status_string", "layer_args"]
+__all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "gemm_workspace_bytes", "gemm", "AqlmError",
+           "status_string", "layer_args"]
 
 
 def _stream_handle(stream) -> int:
@@ -121,4 +124,33 @@ def gemm_small_batch(codes, codebooks, scales, x, *, out=None, stream=None) -> t
     st = _lib.load().aqlm_gemm_small_batch(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in,
                                            M, B, g, n, x.data_ptr(), out.data_ptr(), _stream_handle(stream))
     _check(st, "aqlm_gemm_small_batch")
+    return out
+
+
+def gemm_workspace_bytes(codes, codebooks, scales, n: int) -> int:
+    """Bytes of device workspace :func:`gemm` needs for n activation rows (0: none)."""
+    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    return int(_lib.load().aqlm_gemm_workspace_bytes(d_out, d_in, M, B, g, int(n)))
+
+
+def gemm(codes, codebooks, scales, x, *, workspace=None, out=None, stream=None) -> torch.Tensor:
+    """Y [n, d_out] = X W^T like :func:`gemm_small_batch`, through ``aqlm_gemm``.
+    ``workspace``: a GPU tensor of at least :func:`gemm_workspace_bytes` bytes;
+    allocated here (by torch) when not given and needed."""
+    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    if x.dtype != torch.float16 or x.dim() != 2 or x.shape[1] != d_in or not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous fp16 GPU tensor [n, d_in]")
+    n = x.shape[0]
+    need = int(_lib.load().aqlm_gemm_workspace_bytes(d_out, d_in, M, B, g, n))
+    if workspace is None and need > 0:
+        workspace = torch.empty((need,), dtype=torch.uint8, device=codes.device)
+    if workspace is not None and (not workspace.is_cuda or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous GPU tensor")
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    if out is None:
+        out = torch.empty((n, d_out), dtype=torch.float16, device=codes.device)
+    st = _lib.load().aqlm_gemm(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in, M, B, g, n,
+                               x.data_ptr(), out.data_ptr(), ws_ptr, ws_bytes, _stream_handle(stream))
+    _check(st, "aqlm_gemm")
     return out

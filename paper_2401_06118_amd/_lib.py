@@ -16,8 +16,9 @@ LIB_PATH = os.path.join(HERE, "libaqlm_mi355x.so")
 
 AQLM_OK = 0
 STATUS_NAMES = {0: "AQLM_OK", 1: "AQLM_ERR_NULL", 2: "AQLM_ERR_SHAPE", 3: "AQLM_ERR_UNSUPPORTED",
-                4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP"}
-EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemm_small_batch", "aqlm_status_string")
+                4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP", 6: "AQLM_ERR_WORKSPACE"}
+EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemm_small_batch",
+           "aqlm_gemm_workspace_bytes", "aqlm_gemm", "aqlm_status_string")
 MAX_GROUPED = 8
 
 
@@ -59,6 +60,10 @@ def load():
         lib.aqlm_gemv_grouped.restype = ctypes.c_int
         lib.aqlm_gemm_small_batch.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p]
         lib.aqlm_gemm_small_batch.restype = ctypes.c_int
+        lib.aqlm_gemm_workspace_bytes.argtypes = [i64, i64, i32, i32, i32, i64]
+        lib.aqlm_gemm_workspace_bytes.restype = ctypes.c_size_t
+        lib.aqlm_gemm.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p, ctypes.c_size_t, p]
+        lib.aqlm_gemm.restype = ctypes.c_int
         lib.aqlm_status_string.argtypes = [ctypes.c_int]
         lib.aqlm_status_string.restype = ctypes.c_char_p
         _lib = lib

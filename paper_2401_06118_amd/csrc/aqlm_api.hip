@@ -57,6 +57,19 @@ int status_of(hipError_t e) { return e == hipSuccess ? AQLM_OK : AQLM_ERR_HIP; }
 // Above this many tokens the dequantize-then-multiply prefill kernel is used.
 constexpr int64_t kSmallBatchMax = 16;
 
+// From this many tokens aqlm_gemm dequantizes the whole matrix into the
+// caller's workspace once and runs the dense product (when d_in allows it).
+constexpr int64_t kTwoPassMin = 64;
+
+bool two_pass(int64_t d_in, int64_t n) { return n >= kTwoPassMin && aqlm::gemm_f16_supported((int32_t)d_in); }
+
+int check_tokens(const uint16_t* x, uint16_t* y, int64_t n, int64_t d_in) {
+  if (!x || !y) return AQLM_ERR_NULL;
+  if (n <= 0 || n >= (int64_t(1) << 31) || n * d_in >= (int64_t(1) << 40)) return AQLM_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
+  return AQLM_OK;
+}
+
 // n = 1: the matrix-core kernel for M in {1, 2, 4} (B = 8) and 1x16 when x
 // fits in its LDS staging (d_in up to 32768 for 8-bit codes, 65536 for
 // 16-bit); the vector-ALU kernel otherwise.
@@ -90,16 +103,13 @@ int aqlm_gemv(const void* codes, const uint16_t* codebooks, const uint16_t* scal
   return status_of(gemv_dispatch(L, x, y, static_cast<hipStream_t>(stream)));
 }
 
-int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
-                          int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
-                          void* stream) {
-  aqlm::Layer L;
-  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
-  if (st != AQLM_OK) return st;
-  if (!x || !y) return AQLM_ERR_NULL;
-  if (n <= 0 || n >= (int64_t(1) << 31) || n * d_in >= (int64_t(1) << 40)) return AQLM_ERR_SHAPE;
-  if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+}  // extern "C"
+
+namespace {
+
+// Workspace-free product with n activation rows (arguments validated).
+int gemm_dispatch(const aqlm::Layer& L, int64_t n, const uint16_t* x, uint16_t* y, hipStream_t s) {
+  const int64_t d_in = L.d_in, d_out = L.d_out;
   if (n == 1) return status_of(gemv_dispatch(L, x, y, s));
   // 2..16 tokens with M = 2 or 4 8-bit codebooks: the matrix-vector kernel's
   // scheme with one MFMA column per token; otherwise the tiled kernel.
@@ -114,6 +124,48 @@ int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const ui
     if (e != hipSuccess) return AQLM_ERR_HIP;
   }
   return AQLM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                          int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
+                          void* stream) {
+  aqlm::Layer L;
+  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  st = check_tokens(x, y, n, d_in);
+  if (st != AQLM_OK) return st;
+  return gemm_dispatch(L, n, x, y, static_cast<hipStream_t>(stream));
+}
+
+size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n) {
+  (void)M;
+  (void)B;
+  if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0 || n <= 0) return 0;
+  if (!two_pass(d_in, n)) return 0;
+  return (size_t)d_out * (size_t)d_in * sizeof(uint16_t);
+}
+
+int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
+              int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y, void* workspace,
+              size_t workspace_bytes, void* stream) {
+  aqlm::Layer L;
+  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  st = check_tokens(x, y, n, d_in);
+  if (st != AQLM_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!two_pass(d_in, n)) return gemm_dispatch(L, n, x, y, s);
+  if (!workspace) return AQLM_ERR_NULL;
+  if (workspace_bytes < (size_t)d_out * (size_t)d_in * sizeof(uint16_t)) return AQLM_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return AQLM_ERR_ALIGN;
+  uint16_t* w = static_cast<uint16_t*>(workspace);
+  const hipError_t e = aqlm::launch_dequant(L, w, s);
+  if (e != hipSuccess) return AQLM_ERR_HIP;
+  return status_of(aqlm::launch_gemm_f16(x, w, y, (int32_t)n, L.d_out, L.d_in, s));
 }
 
 int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
@@ -152,6 +204,7 @@ const char* aqlm_status_string(int status) {
     case AQLM_ERR_UNSUPPORTED: return "unsupported (M, B, g)";
     case AQLM_ERR_ALIGN: return "misaligned pointer";
     case AQLM_ERR_HIP: return "HIP runtime error";
+    case AQLM_ERR_WORKSPACE: return "workspace too small";
   }
   return "unknown status";
 }

@@ -12,13 +12,13 @@ from paper_2401_06118_amd import _lib
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "aqlm.h")
 
-OK, NULL, SHAPE, UNSUP, ALIGN = 0, 1, 2, 3, 4
+OK, NULL, SHAPE, UNSUP, ALIGN, WORKSPACE = 0, 1, 2, 3, 4, 6
 P = 0x10000  # a 64 KiB-aligned fake device address; never dereferenced on error paths
 
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^(?:int|const char\*)\s+(aqlm_\w+)\s*\(", text, flags=re.M)))
+    return sorted(set(re.findall(r"^(?:int|size_t|const char\*)\s+(aqlm_\w+)\s*\(", text, flags=re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -40,7 +40,7 @@ def test_library_exports_every_declared_function(lib):
 
 
 def test_status_strings(lib):
-    for st in range(6):
+    for st in range(7):
         assert lib.aqlm_status_string(st)
     assert lib.aqlm_status_string(99) == b"unknown status"
 
@@ -57,7 +57,13 @@ def deq(lib, codes=P, cb=P, sc=P, d_out=64, d_in=64, M=2, B=8, g=8, w=P):
     return lib.aqlm_dequantize(codes, cb, sc, d_out, d_in, M, B, g, w, None)
 
 
-@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+def gemm_ws(lib, n=64, codes=P, cb=P, sc=P, d_out=64, d_in=64, M=2, B=8, g=8, x=P, y=P, ws=P, ws_bytes=1 << 20):
+    """aqlm_gemm at n = 64 (the workspace path) - every case below fails its
+    checks before anything is launched."""
+    return lib.aqlm_gemm(codes, cb, sc, d_out, d_in, M, B, g, n, x, y, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("fn", [gemv, gemm, deq, gemm_ws])
 def test_null_pointers(lib, fn):
     for kw in ("codes", "cb", "sc"):
         assert fn(lib, **{kw: None}) == NULL
@@ -68,7 +74,7 @@ def test_null_pointers(lib, fn):
         assert fn(lib, y=None) == NULL
 
 
-@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+@pytest.mark.parametrize("fn", [gemv, gemm, deq, gemm_ws])
 def test_shapes(lib, fn):
     assert fn(lib, d_out=0) == SHAPE
     assert fn(lib, d_out=-3) == SHAPE
@@ -82,7 +88,7 @@ def test_gemm_batch_size(lib):
     assert gemm(lib, n=-1) == SHAPE
 
 
-@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+@pytest.mark.parametrize("fn", [gemv, gemm, deq, gemm_ws])
 def test_unsupported_formats(lib, fn):
     assert fn(lib, g=4, d_in=64) == UNSUP
     assert fn(lib, M=0) == UNSUP
@@ -92,7 +98,7 @@ def test_unsupported_formats(lib, fn):
     assert fn(lib, M=1, B=4) == UNSUP
 
 
-@pytest.mark.parametrize("fn", [gemv, gemm, deq])
+@pytest.mark.parametrize("fn", [gemv, gemm, deq, gemm_ws])
 def test_alignment(lib, fn):
     assert fn(lib, codes=P + 1) == ALIGN
     assert fn(lib, cb=P + 8) == ALIGN
@@ -128,3 +134,21 @@ def test_grouped_validation(lib):
     assert lib.aqlm_gemv_grouped(bad, 2, 2, 8, 8, None) == NULL
     bad = (Prob * 2)(good, Prob(P, P, P, P + 2, P, 64, 64))
     assert lib.aqlm_gemv_grouped(bad, 2, 2, 8, 8, None) == ALIGN
+
+
+def test_gemm_workspace(lib):
+    """The workspace path: size query, and a missing, small or misaligned
+    workspace is refused before anything is launched."""
+    need = 64 * 64 * 2
+    assert lib.aqlm_gemm_workspace_bytes(64, 64, 2, 8, 8, 64) == need
+    assert lib.aqlm_gemm_workspace_bytes(64, 64, 1, 16, 8, 1000) == need
+    assert lib.aqlm_gemm_workspace_bytes(11008, 4096, 4, 8, 8, 2048) == 11008 * 4096 * 2
+    assert lib.aqlm_gemm_workspace_bytes(64, 64, 2, 8, 8, 63) == 0      # few rows: no workspace
+    assert lib.aqlm_gemm_workspace_bytes(64, 72, 2, 8, 8, 64) == 0      # d_in not a multiple of 64
+    assert lib.aqlm_gemm_workspace_bytes(0, 64, 2, 8, 8, 64) == 0       # invalid sizes
+    assert lib.aqlm_gemm_workspace_bytes(64, 60, 2, 8, 8, 64) == 0
+    assert lib.aqlm_gemm_workspace_bytes(64, 64, 2, 8, 8, 0) == 0
+    assert gemm_ws(lib, ws=None) == NULL
+    assert gemm_ws(lib, ws_bytes=need - 1) == WORKSPACE
+    assert gemm_ws(lib, ws=P + 8) == ALIGN
+    assert gemm_ws(lib, n=0) == SHAPE

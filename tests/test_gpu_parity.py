@@ -253,6 +253,61 @@ def test_gemv_wide_layers(d_out, d_in, M, B):
     check_products(lay, fp16_to_np(y2)[None])
 
 
+# ------------------------------------------------- workspace product (aqlm_gemm)
+
+@pytest.mark.parametrize("d_out,d_in,M,B,n", [
+    (1000, 4096, 2, 8, 64), (300, 1024, 4, 8, 300), (129, 512, 1, 16, 257), (4096, 4160, 1, 16, 100),
+    (130, 1024, 3, 8, 65), (257, 512, 8, 8, 513), (1, 64, 2, 8, 64), (64, 64, 1, 8, 1000),
+])
+def test_gemm_workspace_matches_oracle(d_out, d_in, M, B, n):
+    """Two-pass path: ragged token and row tiles, every format (the weights
+    are rebuilt by the dequantization kernel, so M = 3 and 8 work too)."""
+    print(f"[gemm-ws] {d_out}x{d_in} M={M} B={B} n={n}", flush=True)
+    lay = synth.layer(8200 + d_out + d_in + M + B + n, d_out, d_in, M, B, n=n)
+    codes, cb, sc, x = to_device(lay)
+    need = aq().gemm_workspace_bytes(codes, cb, sc, n)
+    assert need == d_out * d_in * 2
+    ws = torch.full((need,), 0xAB, dtype=torch.uint8, device="cuda")
+    y = aq().gemm(codes, cb, sc, x, workspace=ws)
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y))
+    # the workspace holds the dequantized weights afterwards, bit for bit
+    w = ws.view(torch.float16).view(d_out, d_in).cpu().numpy().view(np.uint16)
+    assert_bits_equal(w, oracle.dequantize(lay.codes, lay.codebooks, lay.scales))
+
+
+@pytest.mark.parametrize("n", [2048])
+@pytest.mark.parametrize("M,B", [(1, 16), (4, 8)])
+def test_gemm_workspace_prefill_layer_sampled_rows(n, M, B):
+    """11008 x 4096 with 2048 activation rows (the prefill workload), sampled
+    output rows against the oracle."""
+    print(f"[gemm-ws prefill] n={n} M={M} B={B}", flush=True)
+    lay = synth.layer(7000 + n + M, 11008, 4096, M, B, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y = fp16_to_np(aq().gemm(codes, cb, sc, x))
+    rows = np.unique(np.concatenate([[0, 11007], np.random.default_rng(3).integers(0, 11008, 40)]))
+    check_products(lay, y, rows)
+
+
+@pytest.mark.parametrize("d_out,d_in,M,B,n", [(300, 1040, 2, 8, 63), (300, 1040, 4, 8, 200), (200, 1024, 2, 8, 16)])
+def test_gemm_without_workspace_is_small_batch(d_out, d_in, M, B, n):
+    """When the size query says 0 the call is exactly aqlm_gemm_small_batch
+    (bit for bit) and takes no workspace."""
+    lay = synth.layer(8300 + d_in + n, d_out, d_in, M, B, n=n)
+    codes, cb, sc, x = to_device(lay)
+    assert aq().gemm_workspace_bytes(codes, cb, sc, n) == 0
+    y1 = aq().gemm(codes, cb, sc, x).cpu().numpy().view(np.uint16)
+    y2 = aq().gemm_small_batch(codes, cb, sc, x).cpu().numpy().view(np.uint16)
+    assert np.array_equal(y1, y2)
+
+
+def test_gemm_workspace_deterministic():
+    lay = synth.layer(16, 700, 2048, 2, 8, n=300)
+    codes, cb, sc, x = to_device(lay)
+    ys = [aq().gemm(codes, cb, sc, x).cpu().numpy().view(np.uint16) for _ in range(3)]
+    assert all(np.array_equal(ys[0], v) for v in ys[1:])
+
+
 def test_gemm_small_batch_deterministic():
     lay = synth.layer(14, 3000, 4096, 4, 8, n=8)
     codes, cb, sc, x = to_device(lay)
