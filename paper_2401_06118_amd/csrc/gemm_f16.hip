@@ -8,9 +8,9 @@
 // (8 consecutive K values per lane), so no transposition is needed anywhere.
 //
 // Workgroup: 512 threads (8 waves, 2 along tokens x 4 along rows), a tile of
-// BM tokens x BN rows, K-steps of 64.  Each step's X and W rows are copied
-// global -> registers -> LDS one step ahead (double-buffered stages), one
-// barrier per step.  LDS rows are 128 bytes (eight 16-byte chunks) with the
+// BM tokens x BN rows, K-steps of 64.  Each step's X and W rows are loaded
+// into registers three steps ahead and stored into one of two LDS stages
+// one step ahead, one barrier per step.  LDS rows are 128 bytes (eight 16-byte chunks) with the
 // chunk index XORed by bits 1..3 of the row, so that the fragment reads of 16
 // consecutive rows, and the stores of two consecutive rows, hit 16 different
 // bank quads without padding.
@@ -21,18 +21,21 @@ namespace aqlm {
 
 namespace {
 
-constexpr int kGfThreads = 512;
 constexpr int kGfK = 64;  // reduction elements per step (two K32 MFMA halves)
 
-template <int FM, int FN>  // per wave: FM 16-token blocks x FN 16-row blocks
+// WM x WN waves; each wave owns FM 16-token blocks x FN 16-row blocks.
+template <int WM, int WN, int FM, int FN>
 struct GfCfg {
-  static constexpr int kBM = 2 * FM * 16;  // tokens per workgroup
-  static constexpr int kBN = 4 * FN * 16;  // weight rows per workgroup
-  static constexpr int kRows = kBM + kBN;  // LDS rows per stage: tokens, then weight rows
+  static constexpr int kThreads = WM * WN * kWave;
+  static constexpr int kBM = WM * FM * 16;  // tokens per workgroup
+  static constexpr int kBN = WN * FN * 16;  // weight rows per workgroup
+  static constexpr int kRows = kBM + kBN;   // LDS rows per stage: tokens, then weight rows
   static constexpr int kStageU4 = kRows * 8;
-  static constexpr int kLoads = kRows * 8 / kGfThreads;  // 16-byte loads per thread per step
+  static constexpr int kRowsPerLoad = kThreads / 8;  // stage rows one load round covers
+  static constexpr int kLoads = kRows / kRowsPerLoad;  // 16-byte loads per thread per step
   static constexpr size_t kLds = 2 * (size_t)kStageU4 * 16;
-  static_assert(kBM % 64 == 0 && kBN % 64 == 0, "a load round (64 rows) is all tokens or all weight rows");
+  static_assert(kBM % kRowsPerLoad == 0 && kBN % kRowsPerLoad == 0,
+                "a load round is all tokens or all weight rows");
 };
 
 // LDS position (in 16-byte units) of chunk c of stage row r.
@@ -48,15 +51,15 @@ struct GemmF16Args {
   int32_t tok_tiles;
 };
 
-template <int FM, int FN>
-__global__ __launch_bounds__(kGfThreads) void k_gemm_f16(const GemmF16Args a) {
-  using P = GfCfg<FM, FN>;
+template <int WM, int WN, int FM, int FN>
+__global__ __launch_bounds__(WM * WN * kWave) void k_gemm_f16(const GemmF16Args a) {
+  using P = GfCfg<WM, WN, FM, FN>;
   extern __shared__ uint4 lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int r16 = lane & 15, slot = lane >> 4;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % WM, wn = wave / WM;
   // Workgroup b takes token tile b % tok_tiles: the workgroups are dealt to
   // the 8 XCDs round-robin, so each XCD's L2 keeps its token tiles' X while
   // the weight tiles stream past.
@@ -65,14 +68,14 @@ __global__ __launch_bounds__(kGfThreads) void k_gemm_f16(const GemmF16Args a) {
   const int32_t KU = a.K / 8;  // 16-byte chunks per row
   const int ksteps = a.K / kGfK;
 
-  // Load j of this thread: stage row r = tid / 8 + 64 j, chunk tid % 8.  Rows
+  // Load j of this thread: stage row r = tid / 8 + kRowsPerLoad j, chunk tid % 8.  Rows
   // past the end read the last valid row (their results are not stored).
   const int lc = tid & 7;
   const uint4* src[P::kLoads];
   int dst[P::kLoads];
 #pragma unroll
   for (int j = 0; j < P::kLoads; ++j) {
-    const int r = (tid >> 3) + 64 * j;
+    const int r = (tid >> 3) + P::kRowsPerLoad * j;
     if (r < P::kBM) {
       int32_t t = tok0 + r;
       t = t < a.n ? t : a.n - 1;
@@ -90,28 +93,30 @@ __global__ __launch_bounds__(kGfThreads) void k_gemm_f16(const GemmF16Args a) {
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = f4_t{0.f, 0.f, 0.f, 0.f};
 
-  // (chunks move as u32x4_t: copies of uint4 from global memory stay in
-  // scratch memory instead of registers)
+  // Chunks move as u32x4_t (copies of uint4 from global memory would stay in
+  // scratch memory instead of registers).  Loads run kDepth steps ahead of
+  // their store into LDS, in kDepth register sets: set s holds the step j
+  // with j % kDepth == s.  A step past the last reloads the last one, so
+  // every load is unconditional and the wait before each store counts
+  // exactly the loads issued after it.
+  constexpr int kDepth = 3;
   u32x4_t* lds4 = reinterpret_cast<u32x4_t*>(lds);
-  {
-    u32x4_t st[P::kLoads];
+  u32x4_t st[kDepth][P::kLoads];
+  auto g_load = [&](int k, auto set) {
+    constexpr int sidx = decltype(set)::value;
+    const int kc = (k < ksteps ? k : ksteps - 1) * (kGfK / 8);
 #pragma unroll
-    for (int j = 0; j < P::kLoads; ++j) st[j] = *reinterpret_cast<const u32x4_t*>(src[j]);
+    for (int j = 0; j < P::kLoads; ++j) st[sidx][j] = *reinterpret_cast<const u32x4_t*>(src[j] + kc);
+  };
+  auto l_store = [&](int k, auto set) {
+    constexpr int sidx = decltype(set)::value;
+    u32x4_t* stage = lds4 + (k & 1) * P::kStageU4;
 #pragma unroll
-    for (int j = 0; j < P::kLoads; ++j) lds4[dst[j]] = st[j];
-  }
-  __syncthreads();
+    for (int j = 0; j < P::kLoads; ++j) stage[dst[j]] = st[sidx][j];
+  };
   const int xr0 = wm * FM * 16 + r16;          // this lane's token row in the stage
   const int wr0 = P::kBM + wn * FN * 16 + r16;  // this lane's weight row in the stage
-  for (int k = 0; k < ksteps; ++k) {
-    // Step k + 1's chunks (past the last step the last one is reloaded, so
-    // every load is unconditional and the wait before each store is exact);
-    // the scheduling barrier keeps them ahead of this step's multiplies.
-    const int kn = (k + 1 < ksteps ? k + 1 : k) * (kGfK / 8);
-    u32x4_t st[P::kLoads];
-#pragma unroll
-    for (int j = 0; j < P::kLoads; ++j) st[j] = *reinterpret_cast<const u32x4_t*>(src[j] + kn);
-    __builtin_amdgcn_sched_barrier(0);
+  auto compute = [&](int k) {
     const u32x4_t* stage = lds4 + (k & 1) * P::kStageU4;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -127,13 +132,30 @@ __global__ __launch_bounds__(kGfThreads) void k_gemm_f16(const GemmF16Args a) {
         for (int fn = 0; fn < FN; ++fn)
           acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xf[fm], wf[fn], acc[fm][fn], 0, 0, 0);
     }
-    if (k + 1 < ksteps) {  // stage (k+1)&1 was last read before the previous barrier
-      u32x4_t* next = lds4 + ((k + 1) & 1) * P::kStageU4;
-#pragma unroll
-      for (int j = 0; j < P::kLoads; ++j) next[dst[j]] = st[j];
-    }
+  };
+  // Step k (register set of step k + 1: NEXT): multiply stage k & 1, store
+  // step k + 1 into the other stage (last read before the previous barrier),
+  // then reuse NEXT for the loads of step k + 1 + kDepth.
+  auto step = [&](int k, auto next) {
+    compute(k);
+    if (k + 1 < ksteps) l_store(k + 1, next);
+    g_load(k + 1 + kDepth, next);
     __syncthreads();
+  };
+  g_load(0, IntC<0>{});
+  g_load(1, IntC<1>{});
+  g_load(2, IntC<2>{});
+  l_store(0, IntC<0>{});
+  g_load(3, IntC<0>{});
+  __syncthreads();
+  int k = 0;
+  for (; k + 3 <= ksteps; k += 3) {
+    step(k, IntC<1>{});
+    step(k + 1, IntC<2>{});
+    step(k + 2, IntC<0>{});
   }
+  if (k < ksteps) step(k, IntC<1>{});
+  if (k + 1 < ksteps) step(k + 1, IntC<2>{});
 
   // D[token][row]: lane holds row r16 of its block and tokens 4 * slot + e.
 #pragma unroll
@@ -150,12 +172,12 @@ __global__ __launch_bounds__(kGfThreads) void k_gemm_f16(const GemmF16Args a) {
   }
 }
 
-template <int FM, int FN>
+template <int WM, int WN, int FM, int FN>
 hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t n, int32_t d_out, int32_t K,
                         hipStream_t s) {
-  using P = GfCfg<FM, FN>;
+  using P = GfCfg<WM, WN, FM, FN>;
   static_assert(P::kLds <= 160 * 1024, "LDS budget");
-  auto kern = k_gemm_f16<FM, FN>;
+  auto kern = k_gemm_f16<WM, WN, FM, FN>;
   static bool attr_set = false;  // set once per kernel; a repeated set is harmless
   if (!attr_set) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -171,7 +193,7 @@ hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32
     const int32_t tok_tiles = (nt + P::kBM - 1) / P::kBM;
     const GemmF16Args a{reinterpret_cast<const uint4*>(x + t0 * K), reinterpret_cast<const uint4*>(w), y + t0 * d_out,
                         nt, d_out, K, tok_tiles};
-    hipLaunchKernelGGL(kern, dim3((uint32_t)(row_tiles * tok_tiles)), dim3(kGfThreads), P::kLds, s, a);
+    hipLaunchKernelGGL(kern, dim3((uint32_t)(row_tiles * tok_tiles)), dim3(P::kThreads), P::kLds, s, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -182,14 +204,14 @@ hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32
 
 bool gemm_f16_supported(int32_t d_in) { return d_in % kGfK == 0; }
 
-// Tile choice: 256 tokens x 128 rows; 128 x 128 when that leaves fewer than
-// two tiles per CU.
+// Tile: 128 tokens x 128 rows (8 waves of 64 x 32, two workgroups per CU).
+// Measured at 256 and 2048 x 11008 x 4096: 256 x 128, 128 x 256 and 4-wave
+// tiles were as fast or slower, and 64 x 128 tiles (more workgroups for few
+// tokens) took 88 us against 50 us at 256 tokens.
 hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t n, int32_t d_out, int32_t K,
                            hipStream_t s) {
   if (K % kGfK != 0 || n < 1 || d_out < 1) return hipErrorInvalidValue;
-  const int64_t big = ((n + 255) / 256) * (int64_t)((d_out + 127) / 128);
-  if (big >= 2 * num_cus()) return run_gemm_f16<8, 2>(x, w, y, n, d_out, K, s);
-  return run_gemm_f16<4, 2>(x, w, y, n, d_out, K, s);
+  return run_gemm_f16<2, 4, 4, 2>(x, w, y, n, d_out, K, s);
 }
 
 }  // namespace aqlm
