@@ -9,7 +9,7 @@
 //
 // Workgroup: 512 threads (8 waves, 2 along tokens x 4 along rows), a tile of
 // BM tokens x BN rows, K-steps of 64.  Each step's X and W rows are loaded
-// into registers three steps ahead and stored into one of two LDS stages
+// into registers two steps ahead and stored into one of two LDS stages
 // one step ahead, one barrier per step.  LDS rows are 128 bytes (eight 16-byte chunks) with the
 // chunk index XORed by bits 1..3 of the row, so that the fragment reads of 16
 // consecutive rows, and the stores of two consecutive rows, hit 16 different
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(WM * WN * kWave) void k_gemm_f16(const GemmF16Args 
   // with j % kDepth == s.  A step past the last reloads the last one, so
   // every load is unconditional and the wait before each store counts
   // exactly the loads issued after it.
-  constexpr int kDepth = 3;
+  constexpr int kDepth = 2;  // three sets measured 2-3 % slower (more registers)
   u32x4_t* lds4 = reinterpret_cast<u32x4_t*>(lds);
   u32x4_t st[kDepth][P::kLoads];
   auto g_load = [&](int k, auto set) {
@@ -142,20 +142,35 @@ __global__ __launch_bounds__(WM * WN * kWave) void k_gemm_f16(const GemmF16Args 
     g_load(k + 1 + kDepth, next);
     __syncthreads();
   };
-  g_load(0, IntC<0>{});
-  g_load(1, IntC<1>{});
-  g_load(2, IntC<2>{});
-  l_store(0, IntC<0>{});
-  g_load(3, IntC<0>{});
-  __syncthreads();
-  int k = 0;
-  for (; k + 3 <= ksteps; k += 3) {
-    step(k, IntC<1>{});
-    step(k + 1, IntC<2>{});
-    step(k + 2, IntC<0>{});
+  if constexpr (kDepth == 3) {
+    g_load(0, IntC<0>{});
+    g_load(1, IntC<1>{});
+    g_load(2, IntC<2>{});
+    l_store(0, IntC<0>{});
+    g_load(3, IntC<0>{});
+    __syncthreads();
+    int k = 0;
+    for (; k + 3 <= ksteps; k += 3) {
+      step(k, IntC<1>{});
+      step(k + 1, IntC<2>{});
+      step(k + 2, IntC<0>{});
+    }
+    if (k < ksteps) step(k, IntC<1>{});
+    if (k + 1 < ksteps) step(k + 1, IntC<2>{});
+  } else {
+    static_assert(kDepth == 2, "two or three register sets");
+    g_load(0, IntC<0>{});
+    g_load(1, IntC<1>{});
+    l_store(0, IntC<0>{});
+    g_load(2, IntC<0>{});
+    __syncthreads();
+    int k = 0;
+    for (; k + 2 <= ksteps; k += 2) {
+      step(k, IntC<1>{});
+      step(k + 1, IntC<0>{});
+    }
+    if (k < ksteps) step(k, IntC<1>{});
   }
-  if (k < ksteps) step(k, IntC<1>{});
-  if (k + 1 < ksteps) step(k + 1, IntC<2>{});
 
   // D[token][row]: lane holds row r16 of its block and tokens 4 * slot + e.
 #pragma unroll
@@ -206,8 +221,8 @@ bool gemm_f16_supported(int32_t d_in) { return d_in % kGfK == 0; }
 
 // Tile: 128 tokens x 128 rows (8 waves of 64 x 32, two workgroups per CU).
 // Measured at 256 and 2048 x 11008 x 4096: 256 x 128, 128 x 256 and 4-wave
-// tiles were as fast or slower, and 64 x 128 tiles (more workgroups for few
-// tokens) took 88 us against 50 us at 256 tokens.
+// tiles (64 x 64 per wave) were as fast or slower, and 64 x 128 tiles (more
+// workgroups for few tokens) took 88 us against 50 us at 256 tokens.
 hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t n, int32_t d_out, int32_t K,
                            hipStream_t s) {
   if (K % kGfK != 0 || n < 1 || d_out < 1) return hipErrorInvalidValue;
