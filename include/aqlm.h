@@ -112,9 +112,10 @@ int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t 
  * with W reconstructed as above, fp32 accumulation, any n >= 1 (the batched
  * and prefill products of a layer; the paper times the single-row case,
  * Sec. 4.3).  n = 1 runs the matrix-vector kernel; 2..16 rows put the rows in
- * the matrix-core (MFMA) columns of the same scheme; more rows dequantize
- * weight tiles into on-chip memory once per tile of 128 or 256 rows of x and
- * feed them to dense fp16 MFMA products.  Needs no workspace.  Results are
+ * the matrix-core (MFMA) columns of the same scheme, and up to 64 rows (32
+ * for 1x16) run as chunks of 16; more rows dequantize weight tiles into
+ * on-chip memory once per tile of 128 or 256 rows of x and feed them to dense
+ * fp16 MFMA products.  Needs no workspace.  Results are
  * within fp32-accumulation accuracy of fp16(W) x, not bit-exact with it.
  * Deterministic. */
 int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales,

@@ -54,8 +54,15 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
 
 int status_of(hipError_t e) { return e == hipSuccess ? AQLM_OK : AQLM_ERR_HIP; }
 
-// Above this many tokens the dequantize-then-multiply prefill kernel is used.
+// Above this many tokens the dequantize-then-multiply prefill kernel is used
+// (up to kChunkedMax tokens in chunks of kSmallBatchMax when the small-batch
+// kernel covers the format: its time barely grows up to 16 tokens, while the
+// prefill kernel's is flat from 17 to 256 tokens at about four times that).
 constexpr int64_t kSmallBatchMax = 16;
+constexpr int64_t kChunkedMax = 64;
+// 1x16 takes the general tiled kernel per chunk, whose time grows faster
+// with the token count: chunks pay off up to two of them.
+constexpr int64_t kChunkedMax16 = 32;
 
 // From this many tokens aqlm_gemm dequantizes the whole matrix into the
 // caller's workspace once and runs the dense product (when d_in allows it).
@@ -114,6 +121,16 @@ int gemm_dispatch(const aqlm::Layer& L, int64_t n, const uint16_t* x, uint16_t* 
   // 2..16 tokens with M = 2 or 4 8-bit codebooks: the matrix-vector kernel's
   // scheme with one MFMA column per token; otherwise the tiled kernel.
   if (aqlm::gemm_nb_supported(L, (int32_t)n)) return status_of(aqlm::launch_gemm_nb(L, (int32_t)n, x, y, s));
+  const bool chunk_nb = n <= kChunkedMax && aqlm::gemm_nb_supported(L, (int32_t)kSmallBatchMax);
+  const bool chunk_16 = n <= kChunkedMax16 && L.B == 16 && aqlm::mfma_supported(L);
+  if (n > kSmallBatchMax && (chunk_nb || chunk_16)) {
+    for (int64_t t0 = 0; t0 < n; t0 += kSmallBatchMax) {
+      const int64_t nt = n - t0 < kSmallBatchMax ? n - t0 : kSmallBatchMax;
+      const int st = gemm_dispatch(L, nt, x + t0 * d_in, y + t0 * d_out, s);
+      if (st != AQLM_OK) return st;
+    }
+    return AQLM_OK;
+  }
   // More tokens: dequantized weight tiles feed a dense MFMA product.
   if (n > kSmallBatchMax && aqlm::prefill_supported(L)) return status_of(aqlm::launch_prefill(L, (int32_t)n, x, y, s));
   if (aqlm::mfma_supported(L)) return status_of(aqlm::launch_gemm_mfma(L, (int32_t)n, x, y, s));
