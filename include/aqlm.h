@@ -122,10 +122,13 @@ int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const ui
                           int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n,
                           const uint16_t* x, uint16_t* y, void* stream);
 
-/* Device workspace, in bytes, that aqlm_gemm needs for these sizes: d_out *
- * d_in * 2 (the dequantized weights) when it takes the two-pass path
- * (n >= 64 and d_in a multiple of 64), else 0.  Returns 0 for invalid sizes
- * (aqlm_gemm then reports the error). */
+/* Device workspace, in bytes, that aqlm_gemm needs for these sizes, 0 when
+ * it does not take the two-pass path (it does when n >= 64 and d_in is a
+ * multiple of 64): the dequantized weights (d_out * d_in * 2, rounded up to
+ * 256) and, when the product has fewer 128 x 128 output tiles than the GPU
+ * has compute units and is split along d_in, fp32 partial sums (up to
+ * 8 * n * d_out * 4).  Depends on the current device's compute-unit count.
+ * Returns 0 for invalid sizes (aqlm_gemm then reports the error). */
 size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n);
 
 /* The product of aqlm_gemm_small_batch with a caller-provided workspace:
@@ -135,8 +138,10 @@ size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t
  * accumulation reads them; this removes the per-tile rebuilding of the
  * weights that aqlm_gemm_small_batch pays.  `workspace` is DEVICE memory of
  * at least aqlm_gemm_workspace_bytes(...) bytes, 16-byte aligned, owned by
- * the caller; its contents are overwritten (they hold W afterwards) and it
- * must not alias any other argument.  When the size query returns 0 the
+ * the caller; its contents are overwritten (its first d_out * d_in * 2 bytes
+ * hold W afterwards) and it must not alias any other argument.  A split
+ * product adds the partial sums in a fixed order, so results stay
+ * deterministic.  When the size query returns 0 the
  * workspace is not used and may be NULL, and the call computes exactly what
  * aqlm_gemm_small_batch computes.  Errors as above, plus AQLM_ERR_NULL for a
  * needed NULL workspace and AQLM_ERR_WORKSPACE for a small one.

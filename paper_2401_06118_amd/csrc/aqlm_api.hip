@@ -70,6 +70,12 @@ constexpr int64_t kTwoPassMin = 64;
 
 bool two_pass(int64_t d_in, int64_t n) { return n >= kTwoPassMin && aqlm::gemm_f16_supported((int32_t)d_in); }
 
+// The dequantized weights, rounded up to 256 bytes so that the partial sums
+// that follow them in the workspace stay aligned.
+size_t ws_weight_bytes(int64_t d_out, int64_t d_in) {
+  return ((size_t)d_out * (size_t)d_in * sizeof(uint16_t) + 255) & ~(size_t)255;
+}
+
 int check_tokens(const uint16_t* x, uint16_t* y, int64_t n, int64_t d_in) {
   if (!x || !y) return AQLM_ERR_NULL;
   if (n <= 0 || n >= (int64_t(1) << 31) || n * d_in >= (int64_t(1) << 40)) return AQLM_ERR_SHAPE;
@@ -163,7 +169,7 @@ size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t
   (void)B;
   if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0 || n <= 0) return 0;
   if (!two_pass(d_in, n)) return 0;
-  return (size_t)d_out * (size_t)d_in * sizeof(uint16_t);
+  return ws_weight_bytes(d_out, d_in) + aqlm::gemm_f16_part_bytes(n, d_out, d_in);
 }
 
 int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
@@ -177,12 +183,14 @@ int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scal
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (!two_pass(d_in, n)) return gemm_dispatch(L, n, x, y, s);
   if (!workspace) return AQLM_ERR_NULL;
-  if (workspace_bytes < (size_t)d_out * (size_t)d_in * sizeof(uint16_t)) return AQLM_ERR_WORKSPACE;
+  const size_t wbytes = ws_weight_bytes(d_out, d_in);
+  if (workspace_bytes < wbytes + aqlm::gemm_f16_part_bytes(n, d_out, d_in)) return AQLM_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return AQLM_ERR_ALIGN;
   uint16_t* w = static_cast<uint16_t*>(workspace);
+  float* part = reinterpret_cast<float*>(static_cast<char*>(workspace) + wbytes);
   const hipError_t e = aqlm::launch_dequant(L, w, s);
   if (e != hipSuccess) return AQLM_ERR_HIP;
-  return status_of(aqlm::launch_gemm_f16(x, w, y, (int32_t)n, L.d_out, L.d_in, s));
+  return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, L.d_out, L.d_in, s));
 }
 
 int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,

@@ -45,10 +45,13 @@ struct GemmF16Args {
   const uint4* x;  // [n][K / 8]
   const uint4* w;  // [d_out][K / 8]
   uint16_t* y;     // [n][d_out]
+  float* part;     // [splits][n][d_out] fp32 partial sums when splits > 1
   int32_t n;
   int32_t d_out;
   int32_t K;
   int32_t tok_tiles;
+  int32_t row_tiles;
+  int32_t splits;
 };
 
 template <int WM, int WN, int FM, int FN>
@@ -63,10 +66,18 @@ __global__ __launch_bounds__(WM * WN * kWave) void k_gemm_f16(const GemmF16Args 
   // Workgroup b takes token tile b % tok_tiles: the workgroups are dealt to
   // the 8 XCDs round-robin, so each XCD's L2 keeps its token tiles' X while
   // the weight tiles stream past.
-  const int32_t tok0 = (int32_t)(blockIdx.x % (uint32_t)a.tok_tiles) * P::kBM;
-  const int32_t row0 = (int32_t)(blockIdx.x / (uint32_t)a.tok_tiles) * P::kBN;
+  // With splits > 1 (too few tiles to fill the chip) the K-steps are divided
+  // among `splits` workgroups per tile, each writing fp32 partial sums that
+  // k_splitk_sum adds in a fixed order.
+  const uint32_t b = blockIdx.x;
+  const int32_t tok0 = (int32_t)(b % (uint32_t)a.tok_tiles) * P::kBM;
+  const uint32_t rest = b / (uint32_t)a.tok_tiles;
+  const int32_t row0 = (int32_t)(rest % (uint32_t)a.row_tiles) * P::kBN;
+  const int split = (int)(rest / (uint32_t)a.row_tiles);
   const int32_t KU = a.K / 8;  // 16-byte chunks per row
-  const int ksteps = a.K / kGfK;
+  const int kall = a.K / kGfK;
+  const int ks0 = (int)((int64_t)kall * split / a.splits);
+  const int ksteps = (int)((int64_t)kall * (split + 1) / a.splits) - ks0;
 
   // Load j of this thread: stage row r = tid / 8 + kRowsPerLoad j, chunk tid % 8.  Rows
   // past the end read the last valid row (their results are not stored).
@@ -79,11 +90,11 @@ __global__ __launch_bounds__(WM * WN * kWave) void k_gemm_f16(const GemmF16Args 
     if (r < P::kBM) {
       int32_t t = tok0 + r;
       t = t < a.n ? t : a.n - 1;
-      src[j] = a.x + (size_t)t * KU + lc;
+      src[j] = a.x + (size_t)t * KU + (size_t)ks0 * (kGfK / 8) + lc;
     } else {
       int32_t i = row0 + (r - P::kBM);
       i = i < a.d_out ? i : a.d_out - 1;
-      src[j] = a.w + (size_t)i * KU + lc;
+      src[j] = a.w + (size_t)i * KU + (size_t)ks0 * (kGfK / 8) + lc;
     }
     dst[j] = gf_pos(r, lc);
   }
@@ -182,16 +193,34 @@ __global__ __launch_bounds__(WM * WN * kWave) void k_gemm_f16(const GemmF16Args 
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int32_t t = tok0 + wm * FM * 16 + fm * 16 + 4 * slot + e;
-        if (t < a.n) a.y[(size_t)t * a.d_out + row] = f2h(acc[fm][fn][e]);
+        if (t >= a.n) continue;
+        const size_t o = (size_t)t * a.d_out + row;
+        if (a.splits == 1)
+          a.y[o] = f2h(acc[fm][fn][e]);
+        else
+          a.part[(size_t)split * a.n * a.d_out + o] = acc[fm][fn][e];
       }
   }
 }
 
+// y = fp16(sum over splits of the partial sums), in split order.
+__global__ __launch_bounds__(256) void k_splitk_sum(const float* __restrict__ part, uint16_t* __restrict__ y,
+                                                    int64_t count, int32_t splits) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= count) return;
+  float v = part[i];
+  for (int s = 1; s < splits; ++s) v += part[(size_t)s * count + i];
+  y[i] = f2h(v);
+}
+
+constexpr int kGfBM = 128, kGfBN = 128;  // the tile launched below
+
 template <int WM, int WN, int FM, int FN>
-hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t n, int32_t d_out, int32_t K,
-                        hipStream_t s) {
+hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, float* part, int32_t splits, int32_t n,
+                        int32_t d_out, int32_t K, hipStream_t s) {
   using P = GfCfg<WM, WN, FM, FN>;
   static_assert(P::kLds <= 160 * 1024, "LDS budget");
+  static_assert(P::kBM == kGfBM && P::kBN == kGfBN, "tile size used by gemm_f16_splits");
   auto kern = k_gemm_f16<WM, WN, FM, FN>;
   static bool attr_set = false;  // set once per kernel; a repeated set is harmless
   if (!attr_set) {
@@ -201,13 +230,24 @@ hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32
     attr_set = true;
   }
   const int64_t row_tiles = (d_out + P::kBN - 1) / P::kBN;
+  if (splits > 1) {  // one launch (the size query sized the partials for all n tokens)
+    const int32_t tok_tiles = (n + P::kBM - 1) / P::kBM;
+    const GemmF16Args a{reinterpret_cast<const uint4*>(x), reinterpret_cast<const uint4*>(w), y, part, n, d_out, K,
+                        tok_tiles, (int32_t)row_tiles, splits};
+    hipLaunchKernelGGL(kern, dim3((uint32_t)(row_tiles * tok_tiles * splits)), dim3(P::kThreads), P::kLds, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t count = (int64_t)n * d_out;
+    hipLaunchKernelGGL(k_splitk_sum, dim3((uint32_t)((count + 255) / 256)), dim3(256), 0, s, part, y, count, splits);
+    return hipGetLastError();
+  }
   // token chunks small enough for a one-dimensional grid
   const int64_t chunk = ((int64_t)0x7FFFFFFF / row_tiles) * P::kBM;
   for (int64_t t0 = 0; t0 < n; t0 += chunk) {
     const int32_t nt = (int32_t)(n - t0 < chunk ? n - t0 : chunk);
     const int32_t tok_tiles = (nt + P::kBM - 1) / P::kBM;
     const GemmF16Args a{reinterpret_cast<const uint4*>(x + t0 * K), reinterpret_cast<const uint4*>(w), y + t0 * d_out,
-                        nt, d_out, K, tok_tiles};
+                        nullptr, nt, d_out, K, tok_tiles, (int32_t)row_tiles, 1};
     hipLaunchKernelGGL(kern, dim3((uint32_t)(row_tiles * tok_tiles)), dim3(P::kThreads), P::kLds, s, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -219,14 +259,38 @@ hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32
 
 bool gemm_f16_supported(int32_t d_in) { return d_in % kGfK == 0; }
 
+// K-splits for a product whose 128 x 128 tiles fill at most half of the CUs:
+// doubled while the tiles do not cover the CUs, up to 8 splits and at least
+// 8 K-steps per split.  (At 11008 x 4096 x 256 tokens, 172 tiles on 256 CUs,
+// two splits were slower than none: the partial sums cost more than the
+// idle CUs.)
+int32_t gemm_f16_splits(int64_t n, int64_t d_out, int64_t K) {
+  const int64_t tiles = ((n + kGfBM - 1) / kGfBM) * ((d_out + kGfBN - 1) / kGfBN);
+  const int64_t ksteps = K / kGfK;
+  if (2 * tiles > num_cus()) return 1;
+  // the grid and the partial-sum offsets stay below 2^31 entries per split
+  if (n * d_out >= (int64_t(1) << 31)) return 1;
+  int32_t s = 1;
+  while (tiles * s < num_cus() && s < 8 && ksteps / (2 * s) >= 8) s *= 2;
+  return s;
+}
+
+size_t gemm_f16_part_bytes(int64_t n, int64_t d_out, int64_t K) {
+  const int32_t s = gemm_f16_splits(n, d_out, K);
+  return s > 1 ? (size_t)s * (size_t)n * (size_t)d_out * sizeof(float) : 0;
+}
+
 // Tile: 128 tokens x 128 rows (8 waves of 64 x 32, two workgroups per CU).
 // Measured at 256 and 2048 x 11008 x 4096: 256 x 128, 128 x 256 and 4-wave
 // tiles (64 x 64 per wave) were as fast or slower, and 64 x 128 tiles (more
 // workgroups for few tokens) took 88 us against 50 us at 256 tokens.
-hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t n, int32_t d_out, int32_t K,
-                           hipStream_t s) {
+// `part`: gemm_f16_part_bytes(n, d_out, K) bytes (unused when that is 0).
+hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, float* part, int32_t n, int32_t d_out,
+                           int32_t K, hipStream_t s) {
   if (K % kGfK != 0 || n < 1 || d_out < 1) return hipErrorInvalidValue;
-  return run_gemm_f16<2, 4, 4, 2>(x, w, y, n, d_out, K, s);
+  const int32_t splits = gemm_f16_splits(n, d_out, K);
+  if (splits > 1 && part == nullptr) return hipErrorInvalidValue;
+  return run_gemm_f16<2, 4, 4, 2>(x, w, y, part, splits, n, d_out, K, s);
 }
 
 }  // namespace aqlm

@@ -57,8 +57,10 @@ hipError_t launch_prefill(const Layer& L, int32_t n, const uint16_t* x, uint16_t
 hipError_t launch_gemm_nb(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
 // Dense fp16 product y[t][i] = sum_c x[t][c] w[i][c] (w: dequantized weights).
 bool gemm_f16_supported(int32_t d_in);
-hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, int32_t n, int32_t d_out, int32_t K,
-                           hipStream_t s);
+// fp32 scratch for K-split partial sums (0 when the product is not split).
+size_t gemm_f16_part_bytes(int64_t n, int64_t d_out, int64_t K);
+hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, float* part, int32_t n, int32_t d_out,
+                           int32_t K, hipStream_t s);
 
 int num_cus();
 

@@ -143,6 +143,8 @@ def test_gemm_workspace(lib):
     assert lib.aqlm_gemm_workspace_bytes(64, 64, 2, 8, 8, 64) == need
     assert lib.aqlm_gemm_workspace_bytes(64, 64, 1, 16, 8, 1000) == need
     assert lib.aqlm_gemm_workspace_bytes(11008, 4096, 4, 8, 8, 2048) == 11008 * 4096 * 2
+    # few tiles (32 of 128 x 128 against 256 CUs): split along K in 8, fp32 partials after the weights
+    assert lib.aqlm_gemm_workspace_bytes(4096, 11008, 4, 8, 8, 64) == 4096 * 11008 * 2 + 8 * 64 * 4096 * 4
     assert lib.aqlm_gemm_workspace_bytes(64, 64, 2, 8, 8, 63) == 0      # few rows: no workspace
     assert lib.aqlm_gemm_workspace_bytes(64, 72, 2, 8, 8, 64) == 0      # d_in not a multiple of 64
     assert lib.aqlm_gemm_workspace_bytes(0, 64, 2, 8, 8, 64) == 0       # invalid sizes
