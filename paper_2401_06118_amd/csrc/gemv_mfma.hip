@@ -558,14 +558,46 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     total_bytes += (double)Ls[i].d_out * Ls[i].G * M * (B / 8);
   }
   const int cus = num_cus();
+  // CUs per problem in proportion to its code bytes, at least one each, by
+  // largest remainders so that the shares add up to the CU count: rounding
+  // each share on its own could ask for more workgroups than CUs (Llama-2-70B
+  // q/k/v: 205 + 26 + 26 = 257), and the one extra workgroup then ran after
+  // all the others, doubling the launch.
+  int want_of[kMaxProblems];
+  {
+    double rem[kMaxProblems];
+    int sum = 0;
+    for (int i = 0; i < count; ++i) {
+      const double share = cus * ((double)Ls[i].d_out * Ls[i].G * M * (B / 8)) / total_bytes;
+      want_of[i] = share < 1.0 ? 1 : (int)share;
+      rem[i] = share - (double)want_of[i];
+      sum += want_of[i];
+    }
+    while (sum < cus) {
+      int best = 0;
+      for (int i = 1; i < count; ++i)
+        if (rem[i] > rem[best]) best = i;
+      ++want_of[best];
+      rem[best] -= 1.0;
+      ++sum;
+    }
+    // (the one-CU minimum of tiny problems can overshoot: take it back from
+    // the largest shares)
+    while (sum > cus) {
+      int big = 0;
+      for (int i = 1; i < count; ++i)
+        if (want_of[i] > want_of[big]) big = i;
+      if (want_of[big] <= 1) break;
+      --want_of[big];
+      --sum;
+    }
+  }
   GemvBatch bt{};
   bt.count = count;
   int wg = 0, ni_max = 1, xg_max = 0, rb_max = 1, nks_min = 1 << 30;
   for (int i = 0; i < count; ++i) {
     const Layer& L = Ls[i];
-    const double bytes = (double)L.d_out * L.G * M * (B / 8);
-    int want = (int)(cus * bytes / total_bytes + 0.5);
-    if (want < 1) want = 1;
+    const int want = want_of[i];
     const int64_t cpr = (int64_t)L.G * M;
     const int KS = (int)((cpr + kKS - 1) / kKS);
     // At most rb_cap row blocks per workgroup (accumulator registers and
