@@ -231,7 +231,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
 // x slices of its four code slots once into registers (column-0 lanes
 // only), then runs the RB items (row blocks) of that slice, each into its own
 // accumulator, so no partial sums move until the end.  Code loads run
-// through a ring of D K-slices, all of its items in flight.
+// through a register ring of D K-slices, a few items ahead of their use.
 template <int M, int COPIES, int RB, int D, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   using C = GCfg<8>;
