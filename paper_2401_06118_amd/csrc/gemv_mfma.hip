@@ -236,7 +236,12 @@ template <int M, int COPIES, int RB, int D, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   using C = GCfg<8>;
   constexpr int kXS = C::kCPL / M;  // x slices per code slot per K-slice
-  constexpr int kStep = RB >= 5 ? 2 : 4;  // codewords gathered per block before their MFMAs
+  // codewords gathered per block before their MFMAs (fewer where the
+  // accumulators or, for M = 1, the sixteen x slices take the registers)
+  constexpr int kStep = (RB >= 5 || M == 1) ? 2 : 4;
+  // (the byte-load path of unaligned rows has no registers to spare for it
+  // in its largest layouts)
+  constexpr bool kPinGathers = VEC || (RB < 7 && D < 4);
   // The wave's items run K-slice major, (j, rb) -> item j * RB + rb, through a
   // ring of kSlots code registers (D K-slices of RB blocks).  Consuming an
   // item starts the load of the item kAhead places later (kAhead <= kSlots,
@@ -384,6 +389,10 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
                   bv[u] = lds_load16(cw_addr<M, COPIES>(ring[d][pair ? rb + 1 : rb][t / 4], t % 4, base_m[t % M],
                                                         copy_off + cb_base, t % M));
               }
+              // All the step's gathers go out before its first MFMA.  Left
+              // alone, the scheduler pairs each gather with its MFMA, so every
+              // MFMA waits a full LDS latency.
+              if constexpr (kPinGathers) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
               for (int u = 0; u < kStep; ++u) {
                 const int t = t0 + u;
