@@ -453,6 +453,239 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   }
 }
 
+// 1x16 with the codebook in LDS, one 128 KiB chunk (8192 codewords) at a
+// time.  The 1 MiB codebook does not fit in LDS, and 16-byte gathers from L2
+// run at well under one per clock per CU, so instead the workgroup makes one
+// pass over its codes per chunk (8 passes).  A code outside the current chunk
+// is sent to a zero codeword that follows the chunk in LDS, so every pass runs
+// the same MFMAs and each code adds its product in exactly one pass.  The
+// codes themselves are loaded from HBM once: a wave owns NKS K-slices of the
+// workgroup's RB row blocks (at most 8 items, 32 registers) and keeps them in
+// registers for all passes.  The next chunk is loaded into registers while the
+// current one is in use, then written to LDS between passes.
+constexpr int kCbChunk = 8192;                  // codewords per LDS chunk
+constexpr int kCbPasses = 65536 / kCbChunk;     // chunks of a 16-bit codebook
+constexpr int kCbStage = kCbChunk / kThreads;   // 16-byte chunk loads per thread
+
+// LDS byte addresses of the two codewords of a 32-bit code word in the chunk
+// starting at code `first` (both halves hold `first`): a code outside the
+// chunk gives the zero codeword at entry kCbChunk.  Packed 16-bit arithmetic
+// wraps modulo 2^16, so (code - first) lands in [0, kCbChunk) exactly for the
+// codes of the chunk and above it otherwise.
+__device__ __forceinline__ void cb_chunk_addr(uint32_t word, uint32_t first2, uint32_t base, uint32_t& a0,
+                                              uint32_t& a1) {
+  typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
+  u16x2_t t = __builtin_bit_cast(u16x2_t, word) - __builtin_bit_cast(u16x2_t, first2);
+  t = __builtin_elementwise_min(t, (u16x2_t){(uint16_t)kCbChunk, (uint16_t)kCbChunk});
+  const uint32_t tw = __builtin_bit_cast(uint32_t, t);
+  // base + 16 * half, one v_mad_u32_u16 per code (op_sel picks the high half;
+  // the compiler spends three instructions on each otherwise)
+  asm("v_mad_u32_u16 %0, %1, 16, %2" : "=v"(a0) : "v"(tw), "v"(base));
+  asm("v_mad_u32_u16 %0, %1, 16, %2 op_sel:[1,0,0,0]" : "=v"(a1) : "v"(tw), "v"(base));
+}
+
+template <int NKS, int RB>
+__global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
+  constexpr int kItems = NKS * RB;
+  constexpr int kXG = NKS * kWaves * 32;        // x groups staged (K-slices of 32 groups), zero past G
+  constexpr int kXL = (kXG + kThreads - 1) / kThreads;
+  constexpr int kStep = 2;                      // codewords gathered per block before their MFMAs
+  static_assert(kItems <= 8, "code items are held in registers");
+  extern __shared__ uint4 lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int r16 = lane & 15;
+  const int slot = lane >> 4;
+
+  int p = 0;
+  while (p + 1 < bt.count && bt.p[p + 1].wg_begin <= (int)blockIdx.x) ++p;
+  const uint4* __restrict__ cb = bt.p[p].cb;
+  const uint4* __restrict__ x = bt.p[p].x;
+  const int32_t rows_per_wg = bt.p[p].rows_per_wg;
+  const int32_t row0 = ((int32_t)blockIdx.x - bt.p[p].wg_begin) * rows_per_wg;
+  int32_t rows = bt.p[p].d_out - row0;
+  if (rows > rows_per_wg) rows = rows_per_wg;
+  const int32_t G = bt.p[p].G;
+  const uint32_t pitch = (uint32_t)G * 2u;  // code bytes per row
+  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * pitch;
+
+  uint4* x_lds = lds + kCbChunk + 1;  // after the chunk and its zero codeword
+
+  // 1. loads, in the order they are needed: chunk 0, x, the codes, the scale.
+  // (16-byte values as vector types: a uint4 copy from global goes through
+  // private memory)
+  const u32x4_t* __restrict__ cbv = reinterpret_cast<const u32x4_t*>(cb);
+  u32x4_t stage[kCbStage];
+#pragma unroll
+  for (int k = 0; k < kCbStage; ++k) stage[k] = cbv[tid + k * kThreads];
+  u32x4_t xv[kXL];
+#pragma unroll
+  for (int i = 0; i < kXL; ++i) {
+    const int grp = tid + i * kThreads;
+    xv[i] = u32x4_t{0u, 0u, 0u, 0u};
+    if (grp < G) xv[i] = reinterpret_cast<const u32x4_t*>(x)[grp];
+  }
+  // Item (j, rb): K-slice wave + 16 j of row block rb.  A slot past the row
+  // end (or a whole K-slice past it) reads the row's first bytes instead; x is
+  // zero there.  Rows past the workgroup's last repeat that row; their sums
+  // are never stored.
+  uint32_t cw[kItems][4];
+#pragma unroll
+  for (int j = 0; j < NKS; ++j) {
+    const uint32_t off = (uint32_t)(wave + j * kWaves) * 64u + (uint32_t)slot * 16u;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = rb * 16 + r16 < rows ? rb * 16 + r16 : rows - 1;
+      const uint32_t o = (uint32_t)row * pitch + (off < pitch ? off : 0u);
+      const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) cw[j * RB + rb][e] = v[e];
+    }
+  }
+  const uint16_t sc = bt.p[p].scales[row0 + (tid < rows ? tid : rows - 1)];
+
+  // 2. chunk 0, its zero codeword and x into LDS.
+  u32x4_t* lds_v = reinterpret_cast<u32x4_t*>(lds);
+#pragma unroll
+  for (int k = 0; k < kCbStage; ++k) lds_v[tid + k * kThreads] = stage[k];
+  if (tid == 0) lds_v[kCbChunk] = u32x4_t{0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < kXL; ++i) {
+    const int grp = tid + i * kThreads;
+    if (grp < kXG) reinterpret_cast<u32x4_t*>(x_lds)[grp] = xv[i];
+  }
+  __syncthreads();
+
+  // 3. one pass per chunk.
+  const uint32_t base = (uint32_t)(uintptr_t)lds;
+  f4_t acc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) acc[rb] = f4_t{0.f, 0.f, 0.f, 0.f};
+  f4_t acc_odd = {0.f, 0.f, 0.f, 0.f};  // second chain of an unpaired last block
+  for (int c = 0; c < kCbPasses; ++c) {
+    if (c + 1 < kCbPasses) {
+#pragma unroll
+      for (int k = 0; k < kCbStage; ++k) stage[k] = cbv[(c + 1) * kCbChunk + tid + k * kThreads];
+    }
+    const uint32_t first2 = (uint32_t)(c * kCbChunk) * 0x10001u;
+#pragma unroll
+    for (int j = 0; j < NKS; ++j) {
+      // x group of code t of this lane's slot: K-slice * 32 + slot * 8 + t
+      const uint4* xs = x_lds + (wave + j * kWaves) * 32 + slot * 8;
+      // x for the whole slice where the registers allow, else per step
+      constexpr int kXS = RB <= 2 ? 8 : kStep;
+      uint4 xr[kXS];
+#pragma unroll
+      for (int t0 = 0; t0 < 8; t0 += kStep) {
+        if (t0 % kXS == 0) {
+#pragma unroll
+          for (int u = 0; u < kXS; ++u) xr[u] = xs[t0 + u];
+        }
+        uint4 xb[kStep];
+#pragma unroll
+        for (int u = 0; u < kStep; ++u) xb[u] = xr[(t0 + u) % kXS];
+#pragma unroll
+        for (int rb = 0; rb < RB; rb += 2) {
+          const bool pair = rb + 1 < RB;
+          uint4 av[kStep], bv[kStep];
+#pragma unroll
+          for (int u = 0; u < kStep; u += 2) {
+            const int t = t0 + u;
+            uint32_t a0, a1;
+            cb_chunk_addr(cw[j * RB + rb][t / 2], first2, base, a0, a1);
+            av[u] = lds_load16(a0);
+            av[u + 1] = lds_load16(a1);
+            if (pair) {
+              cb_chunk_addr(cw[j * RB + (pair ? rb + 1 : rb)][t / 2], first2, base, a0, a1);
+              bv[u] = lds_load16(a0);
+              bv[u + 1] = lds_load16(a1);
+            }
+          }
+          // all the step's gathers before its first MFMA
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int u = 0; u < kStep; ++u) {
+            const h8_t xh = __builtin_bit_cast(h8_t, xb[u]);
+            if (pair) {
+              acc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, acc[rb], 0, 0, 0);
+              acc[pair ? rb + 1 : rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                  __builtin_bit_cast(h8_t, bv[u]), xh, acc[pair ? rb + 1 : rb], 0, 0, 0);
+            } else {
+              f4_t& a = (u % 2 == 0) ? acc[rb] : acc_odd;
+              a = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(h8_t, av[u]), xh, a, 0, 0, 0);
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();  // every wave is done with chunk c
+    if (c + 1 < kCbPasses) {
+#pragma unroll
+      for (int k = 0; k < kCbStage; ++k) lds_v[tid + k * kThreads] = stage[k];
+      __syncthreads();
+    }
+  }
+  if constexpr (RB % 2 == 1) acc[RB - 1] += acc_odd;
+
+  // 4. per-wave partials (in the chunk's space, no longer read), then the
+  // fixed-order sum over waves, scale, round, store.
+  float* part = reinterpret_cast<float*>(lds);
+  if (r16 == 0) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) part[(rb * kWaves + wave) * 16 + 4 * slot + e] = acc[rb][e];
+  }
+  __syncthreads();
+  if (tid < rows) {
+    const int rb = tid / 16, rr = tid % 16;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += part[(rb * kWaves + w) * 16 + rr];
+    bt.p[p].y[row0 + tid] = f2h(h2f(sc) * s);
+  }
+}
+
+template <int NKS, int RB>
+hipError_t launch_cb(const GemvBatch& bt, hipStream_t s) {
+  auto kern = k_gemv_cb<NKS, RB>;
+  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
+  if (!attr_set) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const size_t lds = (size_t)(kCbChunk + 1 + NKS * kWaves * 32) * 16;
+  hipLaunchKernelGGL(kern, dim3(bt.total_wgs), dim3(kThreads), lds, s, bt);
+  return hipGetLastError();
+}
+
+// K-slices per wave (NKS) and row blocks per workgroup the chunked 1x16
+// kernel supports: the code items (NKS * RB <= 8) stay in registers, and x
+// (NKS * 8 KiB) fits next to the 128 KiB chunk.
+constexpr int kCbMaxNks = 3;
+constexpr int cb_rb_cap(int nks) { return nks == 1 ? 6 : (nks == 2 ? 4 : 2); }
+
+hipError_t launch_cb_shape(const GemvBatch& bt, int nks, int rb, hipStream_t s) {
+  switch (nks * 8 + rb) {
+    case 8 + 1: return launch_cb<1, 1>(bt, s);
+    case 8 + 2: return launch_cb<1, 2>(bt, s);
+    case 8 + 3: return launch_cb<1, 3>(bt, s);
+    case 8 + 4: return launch_cb<1, 4>(bt, s);
+    case 8 + 5: return launch_cb<1, 5>(bt, s);
+    case 8 + 6: return launch_cb<1, 6>(bt, s);
+    case 16 + 1: return launch_cb<2, 1>(bt, s);
+    case 16 + 2: return launch_cb<2, 2>(bt, s);
+    case 16 + 3: return launch_cb<2, 3>(bt, s);
+    case 16 + 4: return launch_cb<2, 4>(bt, s);
+    case 24 + 1: return launch_cb<3, 1>(bt, s);
+    case 24 + 2: return launch_cb<3, 2>(bt, s);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <int M, int COPIES, int RB, int D, bool VEC>
 hipError_t launch_ks(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
   auto kern = k_gemv_ks<M, COPIES, RB, D, VEC>;
@@ -567,6 +800,21 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     total_bytes += (double)Ls[i].d_out * Ls[i].G * M * (B / 8);
   }
   const int cus = num_cus();
+  // 1x16 runs the chunked-codebook kernel where its code items fit in
+  // registers and x next to the chunk (NKS K-slices per wave).
+  int cb_nks = 0;
+  if (B == 16 && vec) {
+    for (int i = 0; i < count; ++i) {
+      const int KS = (int)(((int64_t)Ls[i].G * 2 + 63) / 64);
+      const int nks = (KS + kWaves - 1) / kWaves;
+      if (nks > cb_nks) cb_nks = nks;
+    }
+    if (cb_nks > kCbMaxNks) cb_nks = 0;
+    // Every workgroup streams the whole codebook through its CU (about 14 us
+    // at the L2 bandwidth), which pays off only above roughly 28 KiB of codes
+    // per CU; smaller launches gather from L2.
+    if (total_bytes < 28.0 * 1024 * cus) cb_nks = 0;
+  }
   // CUs per problem in proportion to its code bytes, at least one each, by
   // largest remainders so that the shares add up to the CU count: rounding
   // each share on its own could ask for more workgroups than CUs (Llama-2-70B
@@ -612,7 +860,7 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     // At most rb_cap row blocks per workgroup (accumulator registers and
     // partial-sum space).  Larger layers run `rounds` workgroups per CU,
     // split evenly rather than leaving a short last round.
-    const int rb_cap = (B == 16) ? kMaxRB : ks_rb_cap(M);
+    const int rb_cap = (B == 16) ? (cb_nks > 0 ? cb_rb_cap(cb_nks) : kMaxRB) : ks_rb_cap(M);
     const int blocks = (L.d_out + 15) / 16;
     const int rounds = (blocks + rb_cap * want - 1) / (rb_cap * want);
     const int rows_per_wg = (L.d_out + want * rounds - 1) / (want * rounds);
@@ -644,6 +892,7 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   if (xg_max > xl * kThreads) return hipErrorInvalidValue;
   const size_t base = (size_t)xg_max * 16 + (size_t)rb_max * kWaves * 16 * 4;
   const size_t limit = 160 * 1024;
+  if (B == 16 && cb_nks > 0) return launch_cb_shape(bt, cb_nks, rb_max, s);
   if (B == 16) {
     if (base > limit) return hipErrorInvalidValue;
     return vec ? launch_copies<1, 16, 0, true>(bt, ni, base, s) : launch_copies<1, 16, 0, false>(bt, ni, base, s);
