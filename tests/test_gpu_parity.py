@@ -125,6 +125,29 @@ def test_gemv_matches_oracle(d_out, d_in, M, B):
     check_products(lay, fp16_to_np(y)[None, :])
 
 
+@pytest.mark.parametrize("shapes", [
+    [(11001, 4096)],            # ragged rows, one K-slice per wave, 3 row blocks per workgroup
+    [(8192, 6144)],             # two K-slices per wave
+    [(5000, 12288)],            # three K-slices per wave (the largest d_in staged next to a chunk)
+    [(5000, 12352)],            # one more K-slice: falls back to the L2 gathers
+    [(11008, 4096)] * 2,        # gate/up: 6 row blocks per workgroup
+    [(4096, 4096), (1024, 4096), (12000, 4096)],  # grouped, above the size threshold together
+])
+def test_gemv_1x16_codebook_chunks(shapes):
+    """1x16 launches large enough for the kernel that stages the codebook in
+    LDS chunk by chunk (eight passes, zero codeword outside the chunk)."""
+    print(f"[gemv-1x16-chunks] {shapes}", flush=True)
+    if len(shapes) == 1:
+        d_out, d_in = shapes[0]
+        lay = synth.layer(9100 + d_out + d_in, d_out, d_in, 1, 16)
+        codes, cb, sc, x = to_device(lay)
+        y = aq().gemv(codes, cb, sc, x[0])
+        torch.cuda.synchronize()
+        check_products(lay, fp16_to_np(y)[None, :])
+    else:
+        _grouped_case(shapes, 1, 16, 9200)
+
+
 def test_gemv_70b_shapes_sampled_rows():
     """Llama-2-70B-shaped 2x8 layers: gate/up 28672 x 8192, down 8192 x 28672,
     k/v 1024 x 8192; outputs checked on sampled rows."""
