@@ -209,7 +209,8 @@ def measured_traffic(kernel_key: str, digest: str):
 
 def cpu_baseline(layers, budget_s):
     """Oracle (dequantize + fp64 product) on the host cores, one layer of each
-    distinct shape, repeated until the budget is spent; scaled to the step."""
+    distinct shape, repeated until the budget is spent; scaled to the step.
+    The two parts are timed separately."""
     import numpy as np
 
     import oracle
@@ -224,18 +225,24 @@ def cpu_baseline(layers, budget_s):
         if L.shape.B == 16:
             codes = codes.view(np.uint16)
         host[key] = (codes, L.codebooks.cpu().numpy(), L.scales.cpu().numpy(), L.x.cpu().numpy())
-        per_shape[key] = []
+        per_shape[key] = ([], [])
     t_end = time.perf_counter() + budget_s
     rounds = 0
     while True:
         for key, (codes, cb, sc, x) in host.items():
             t0 = time.perf_counter()
-            oracle.aqlm_matmul(codes, cb, sc, x)
-            per_shape[key].append(time.perf_counter() - t0)
+            w = oracle.dequantize(codes, cb, sc)
+            t1 = time.perf_counter()
+            oracle.matmul_f16(w, x)
+            t2 = time.perf_counter()
+            per_shape[key][0].append(t1 - t0)
+            per_shape[key][1].append(t2 - t1)
         rounds += 1
         if time.perf_counter() > t_end or rounds >= 50:
             break
-    step_s = sum(len(shapes[k]) * float(np.median(v)) for k, v in per_shape.items())
+    deq_s = sum(len(shapes[k]) * float(np.median(v[0])) for k, v in per_shape.items())
+    mm_s = sum(len(shapes[k]) * float(np.median(v[1])) for k, v in per_shape.items())
+    step_s = deq_s + mm_s
     step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
     return {
         "value": step_bytes / step_s / 1e9,
@@ -245,6 +252,7 @@ def cpu_baseline(layers, budget_s):
         "sample": (f"one layer of each of the {len(shapes)} distinct shapes, dequantize + fp64 product, "
                    f"median of {rounds} runs each, step time = sum over shapes of count x median "
                    f"({step_s:.3f} s per step, {1.0 / step_s:.4f} tok/s-eq)"),
+        "split_s_per_step": {"dequantize": deq_s, "fp64_product": mm_s},
     }
 
 
