@@ -132,6 +132,8 @@ def test_gemv_matches_oracle(d_out, d_in, M, B):
     [(5000, 12352)],            # one more K-slice: falls back to the L2 gathers
     [(11008, 4096)] * 2,        # gate/up: 6 row blocks per workgroup
     [(4096, 4096), (1024, 4096), (12000, 4096)],  # grouped, above the size threshold together
+    [(11008, 4096), (4096, 11008)],                # grouped with different d_in: the first problem's
+                                                   # waves carry two empty K-slices (x zero there)
 ])
 def test_gemv_1x16_codebook_chunks(shapes):
     """1x16 launches large enough for the kernel that stages the codebook in
