@@ -283,7 +283,9 @@ size_t gemm_f16_part_bytes(int64_t n, int64_t d_out, int64_t K) {
 // Tile: 128 tokens x 128 rows (8 waves of 64 x 32, two workgroups per CU).
 // Measured at 256 and 2048 x 11008 x 4096: 256 x 128, 128 x 256 and 4-wave
 // tiles (64 x 64 per wave) were as fast or slower, and 64 x 128 tiles (more
-// workgroups for few tokens) took 88 us against 50 us at 256 tokens.
+// workgroups for few tokens) took 88 us against 50 us at 256 tokens.  The
+// same tile on v_mfma_f32_32x32x16_f16 (waves of 64 x 32 or 64 x 64) was
+// 3-13 % slower at 2048 tokens.
 // `part`: gemm_f16_part_bytes(n, d_out, K) bytes (unused when that is 0).
 hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, float* part, int32_t n, int32_t d_out,
                            int32_t K, hipStream_t s) {
