@@ -12,21 +12,25 @@
 // Work split.  A workgroup (16 waves) owns a range of rows of one problem.  An
 // item is 16 rows x one K-slice of 4 x kCPL codes (kCPL = 16 codes, 16 bytes,
 // per lane); lane (r, s) streams the codes [s*kCPL, s*kCPL + kCPL) of the
-// slice for row r with one 16-byte load.  Two schedules of the items:
-//   k_gemv_mfma (B = 16): items dealt round-robin to the waves, one
-//     accumulator per wave, stored to LDS whenever its row block changes;
+// slice for row r with one 16-byte load.  Three kernels:
+//   k_gemv_mfma (B = 16, small launches): items dealt round-robin to the
+//     waves, one accumulator per wave, stored to LDS whenever its row block
+//     changes; codewords gathered from L2;
 //   k_gemv_ks (B = 8): each wave owns whole K-slices of all the workgroup's
-//     row blocks and keeps one accumulator per block.
-// Either way the per-wave partials are added in a fixed order at the end, so
-// results are deterministic.
+//     row blocks and keeps one accumulator per block;
+//   k_gemv_cb (B = 16, large launches): the k_gemv_ks split with the codes
+//     held in registers, run once per 128 KiB codebook chunk staged in LDS.
+// In every case the per-wave partials are added in a fixed order at the end,
+// so results are deterministic.
 //
 // Memory order.  Vector-memory loads retire in issue order, so the small
 // loads that must finish first (codebooks, x) are issued before the HBM code
 // stream; all NI code loads of a wave are then in flight at once.  While
 // they arrive the codebooks are copied COPIES times into LDS (lane l reads
 // copy l % COPIES, so 16 lanes hit 16 different 16-byte bank quads) and x is
-// staged in LDS, zero-padded to whole K-slices.  B = 16 codebooks (1 MiB)
-// stay in L2 and are gathered with 16-byte global loads.
+// staged in LDS, zero-padded to whole K-slices.  A B = 16 codebook (1 MiB)
+// either stays in L2 and is gathered with 16-byte global loads, or passes
+// through LDS chunk by chunk (k_gemv_cb).
 //
 // Several independent problems with the same (M, B) can share one launch
 // (e.g. the q, k, v projections of a layer): workgroups are dealt to the
