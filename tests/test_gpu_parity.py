@@ -419,3 +419,68 @@ def test_gemv_grouped_error_writes_nothing():
     assert L.load().aqlm_gemv_grouped(arr, 2, 2, 8, 8, None) == 2
     torch.cuda.synchronize()
     assert torch.all(y0 == 5.0) and torch.all(y1 == 5.0)
+
+
+# -------------------------------------------------------- random shapes
+
+def _random_format(rng):
+    """(M, B): every 8-bit codebook count, or 1x16."""
+    if rng.random() < 0.3:
+        return 1, 16
+    return int(rng.integers(1, 9)), 8
+
+
+def _random_d_in(rng, top=1545):
+    """d_in = 8 k up to 8 * (top - 1); 60 % of them multiples of 128, whose
+    code rows are 16-byte aligned for every format (the vector-load paths)."""
+    k = int(rng.integers(1, top))
+    if rng.random() < 0.6:
+        k = max(16, k // 16 * 16)
+    return 8 * k
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_gemv_random_shapes(seed):
+    """Seeded random layers across the dispatch branches: formats, aligned and
+    unaligned code rows, every row-block / K-slice layout, and 1x16 launches
+    on both sides of the codebook-chunk size threshold."""
+    rng = np.random.default_rng(10_000 + seed)
+    M, B = _random_format(rng)
+    d_in = _random_d_in(rng)
+    d_out = int(rng.integers(1, 8001 if B == 16 else 3001))
+    print(f"[gemv-random] seed={seed} d_out={d_out} d_in={d_in} M={M} B={B}", flush=True)
+    lay = synth.layer(11_000 + seed, d_out, d_in, M, B)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemv(codes, cb, sc, x[0])
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y)[None, :])
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_gemv_grouped_random_shapes(seed):
+    """Seeded random groups of 1..8 problems sharing (M, B)."""
+    rng = np.random.default_rng(12_000 + seed)
+    M, B = _random_format(rng)
+    count = int(rng.integers(1, 9))
+    shapes = [(int(rng.integers(1, 2501)), _random_d_in(rng, 1025)) for _ in range(count)]
+    print(f"[grouped-random] seed={seed} M={M} B={B} {shapes}", flush=True)
+    _grouped_case(shapes, M, B, 13_000 + 97 * seed)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_gemm_random_shapes(seed):
+    """Seeded random products with n activation rows through both entry
+    points (the fused small-batch / prefill kernels and the workspace path)."""
+    rng = np.random.default_rng(14_000 + seed)
+    M, B = _random_format(rng)
+    d_in = _random_d_in(rng, 385)                         # up to 3072
+    d_out = int(rng.integers(1, 1201))
+    n = int(rng.integers(2, 161))
+    print(f"[gemm-random] seed={seed} n={n} d_out={d_out} d_in={d_in} M={M} B={B}", flush=True)
+    lay = synth.layer(15_000 + seed, d_out, d_in, M, B, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y1 = aq().gemm_small_batch(codes, cb, sc, x)
+    y2 = aq().gemm(codes, cb, sc, x)
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y1))
+    check_products(lay, fp16_to_np(y2))
