@@ -238,7 +238,7 @@ def cpu_baseline(layers, budget_s):
             per_shape[key][0].append(t1 - t0)
             per_shape[key][1].append(t2 - t1)
         rounds += 1
-        if time.perf_counter() > t_end or rounds >= 50:
+        if time.perf_counter() > t_end or rounds >= 500:
             break
     deq_s = sum(len(shapes[k]) * float(np.median(v[0])) for k, v in per_shape.items())
     mm_s = sum(len(shapes[k]) * float(np.median(v[1])) for k, v in per_shape.items())

@@ -5,6 +5,9 @@
 
 #include <atomic>
 #include <cstdint>
+#include <mutex>
+#include <set>
+#include <tuple>
 
 #include "../../include/aqlm.h"
 #include "launch.h"
@@ -21,6 +24,23 @@ int num_cus() {
   v = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
   cached.store(v, std::memory_order_relaxed);
   return v;
+}
+
+// The dynamic-LDS limit is a per-device property of a kernel: raise it once
+// per (kernel, device, size), under a lock so that concurrent first calls
+// are safe.
+hipError_t allow_dynamic_lds(const void* kern, int bytes) {
+  int dev = 0;
+  const hipError_t d = hipGetDevice(&dev);
+  if (d != hipSuccess) return d;
+  static std::mutex mu;
+  static std::set<std::tuple<const void*, int, int>> done;
+  const std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_tuple(kern, dev, bytes);
+  if (done.count(key)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess) done.insert(key);
+  return e;
 }
 
 }  // namespace aqlm

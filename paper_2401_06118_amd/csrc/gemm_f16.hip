@@ -222,12 +222,9 @@ hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, float
   static_assert(P::kLds <= 160 * 1024, "LDS budget");
   static_assert(P::kBM == kGfBM && P::kBN == kGfBN, "tile size used by gemm_f16_splits");
   auto kern = k_gemm_f16<WM, WN, FM, FN>;
-  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), 160 * 1024);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   const int64_t row_tiles = (d_out + P::kBN - 1) / P::kBN;
   if (splits > 1) {  // one launch (the size query sized the partials for all n tokens)

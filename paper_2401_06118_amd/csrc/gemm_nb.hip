@@ -238,12 +238,9 @@ __global__ __launch_bounds__(kThreadsNB) void k_gemm_nb(const GemmNbArgs a) {
 template <int M, int COPIES, int RB, int D, bool VEC>
 hipError_t launch_nb(const GemmNbArgs& a, int nwg, size_t lds_bytes, hipStream_t s) {
   auto kern = k_gemm_nb<M, COPIES, RB, D, VEC>;
-  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsLimit);
+  {
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), (int)kLdsLimit);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3(nwg), dim3(kThreadsNB), lds_bytes, s, a);
   return hipGetLastError();

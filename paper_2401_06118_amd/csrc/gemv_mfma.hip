@@ -654,12 +654,9 @@ __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
 template <int NKS, int RB>
 hipError_t launch_cb(const GemvBatch& bt, hipStream_t s) {
   auto kern = k_gemv_cb<NKS, RB>;
-  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), 160 * 1024);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   const size_t lds = (size_t)(kCbChunk + 1 + NKS * kWaves * 32) * 16;
   hipLaunchKernelGGL(kern, dim3(bt.total_wgs), dim3(kThreads), lds, s, bt);
@@ -693,12 +690,9 @@ hipError_t launch_cb_shape(const GemvBatch& bt, int nks, int rb, hipStream_t s) 
 template <int M, int COPIES, int RB, int D, bool VEC>
 hipError_t launch_ks(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
   auto kern = k_gemv_ks<M, COPIES, RB, D, VEC>;
-  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), 160 * 1024);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3(bt.total_wgs), dim3(kThreads), lds_bytes, s, bt);
   return hipGetLastError();
@@ -749,12 +743,9 @@ hipError_t launch_ks_rb(const GemvBatch& bt, int rb, int nks, size_t lds_bytes, 
 template <int M, int B, int COPIES, int PF, bool VEC>
 hipError_t launch_pf(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
   auto kern = k_gemv_mfma<M, B, COPIES, PF, VEC>;
-  static bool attr_set = false;  // set once per kernel; a repeated set is harmless
-  if (!attr_set) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+  {
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), 160 * 1024);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3(bt.total_wgs), dim3(kThreads), lds_bytes, s, bt);
   return hipGetLastError();

@@ -63,5 +63,8 @@ hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, fl
                            int32_t K, hipStream_t s);
 
 int num_cus();
+// Allows a kernel `bytes` of dynamic LDS on the current device (once per
+// kernel, device and size).
+hipError_t allow_dynamic_lds(const void* kern, int bytes);
 
 }  // namespace aqlm

@@ -287,12 +287,9 @@ hipError_t run_prefill_bn(const Layer& L, int32_t n, const uint16_t* x, uint16_t
   // 8-byte / 16-byte code loads need every row's code pitch to keep that alignment
   const bool vec = ((int64_t)L.G * M * (B / 8)) % P::kCodeBytes == 0;
   auto kern = vec ? k_prefill<M, B, BN, true> : k_prefill<M, B, BN, false>;
-  static bool attr_set[2] = {false, false};  // per variant; a repeated set is harmless
-  if (!attr_set[vec]) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kPfLdsLimit);
+  {
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), (int)kPfLdsLimit);
     if (e != hipSuccess) return e;
-    attr_set[vec] = true;
   }
   // token chunks small enough for a one-dimensional grid of row x token tiles
   const int64_t row_tiles = (L.d_out + kBM - 1) / kBM;
