@@ -56,7 +56,8 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
   if (g != 8) return AQLM_ERR_UNSUPPORTED;
   if (!((B == 8 && M >= 1 && M <= 8) || (B == 16 && M == 1))) return AQLM_ERR_UNSUPPORTED;
   const int64_t G = d_in / g;
-  if (d_out >= (int64_t(1) << 31) || G >= (int64_t(1) << 31) || d_out * G >= (int64_t(1) << 31))
+  // (sizes and offsets are held in 32 bits on the device side)
+  if (d_out >= (int64_t(1) << 31) || d_in >= (int64_t(1) << 31) || d_out * G >= (int64_t(1) << 31))
     return AQLM_ERR_SHAPE;
   if (!aligned(codes, 16) || !aligned(codebooks, 16) || !aligned(scales, 2)) return AQLM_ERR_ALIGN;
   L->codes = codes;

@@ -81,6 +81,7 @@ def test_shapes(lib, fn):
     assert fn(lib, d_in=0) == SHAPE
     assert fn(lib, d_in=12) == SHAPE          # not a multiple of g
     assert fn(lib, d_out=1 << 20, d_in=1 << 14) == SHAPE  # d_out * d_in/g >= 2^31
+    assert fn(lib, d_out=1, d_in=1 << 31) == SHAPE        # d_in beyond 32 bits
 
 
 def test_gemm_batch_size(lib):
