@@ -30,7 +30,7 @@
  * Supported formats: g = 8 and either B = 8 with 1 <= M <= 8 (M codebooks of
  * 256 entries, e.g. the paper's 2x8 and 4x8 schemes) or B = 16 with M = 1 (one
  * codebook of 65536 entries, the 1x16 scheme).  Sizes: d_out * (d_in / g)
- * must stay below 2^31 and d_out, n below 2^31.
+ * must stay below 2^31 and d_out, d_in, n below 2^31.
  *
  * Alignment: codes, codebooks, x, y and w_out must be 16-byte aligned and
  * scales 2-byte aligned.  Shapes whose code row pitch (d_in/g * M * B/8 bytes)
