@@ -161,6 +161,23 @@ def time_steps(fn, steps, warmup):
     return start.elapsed_time(end) / steps  # ms
 
 
+def step_spread(fn, steps):
+    """Per-step durations from an event pair around each step, in a pass of
+    its own after the timed region (the events between steps would perturb
+    it): p10, median and p90 in ms."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    ts = sorted(a.elapsed_time(b) for a, b in ev)
+    q = lambda f: ts[min(len(ts) - 1, int(f * len(ts)))]
+    return {"p10": q(0.1), "median": q(0.5), "p90": q(0.9), "steps": steps}
+
+
 def per_launch_ms(launches, reps):
     """Average duration of each launch, from a HIP event pair recorded around it
     on the launching (torch current) stream, over `reps` passes.  Each pass
@@ -386,6 +403,7 @@ def main():
     log(f"{args.workload}: {len(layers)} layers in {len(launches)} launches, {step_bytes / 1e9:.3f} GB per step")
     graph = graph_of(launches)
     ms = time_steps(graph.replay, args.steps, args.warmup)
+    spread = step_spread(graph.replay, max(args.steps, 20))
     log(f"step {ms:.4f} ms (graph replay)")
 
     # Dominant kernel: every launch of the step is the matrix-vector kernel
@@ -420,6 +438,7 @@ def main():
             "bytes_per_step": step_bytes,
             "parallelism": "single GPU",
         },
+        "ms_per_step_spread": spread,
         "tokens_per_s_equivalent": 1000.0 / ms,
         "roofline_frac_step": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
         "roofline": {
