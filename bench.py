@@ -281,6 +281,8 @@ def single_layer_rows(aq, torch):
         "4096x4096 1x16": (4096, 4096, 1, 16),
         "11008x4096 1x16": (11008, 4096, 1, 16),
         "4096x11008 1x16": (4096, 11008, 1, 16),
+        "4096x4096 1x15": (4096, 4096, 1, 15),
+        "11008x4096 1x15": (11008, 4096, 1, 15),
         "28672x8192 2x8": (28672, 8192, 2, 8),
     }.items():
         from paper_2401_06118_amd import format as fmt

@@ -20,7 +20,8 @@
  *
  * Layouts (dense, row-major, contiguous):
  *   codes      [d_out][d_in/g][M], m fastest.  uint8_t when B = 8,
- *              uint16_t when B = 16; value = codeword index.
+ *              uint16_t when B = 15 or 16 (unpacked); value = codeword
+ *              index, taken modulo 2^B.
  *   codebooks  [M][2^B][g] fp16 (one codeword = g contiguous values).
  *   scales     [d_out] fp16.
  *   x          [n][d_in] fp16 (n = 1 for the matrix-vector product).
@@ -28,14 +29,17 @@
  *   w_out      [d_out][d_in] fp16.
  *
  * Supported formats: g = 8 and either B = 8 with 1 <= M <= 8 (M codebooks of
- * 256 entries, e.g. the paper's 2x8 and 4x8 schemes) or B = 16 with M = 1 (one
- * codebook of 65536 entries, the 1x16 scheme).  Sizes: d_out * (d_in / g)
- * must stay below 2^31 and d_out, d_in, n below 2^31.
+ * 256 entries, e.g. the paper's 2x8 and 4x8 schemes) or B = 16 or 15 with
+ * M = 1 (one codebook of 65536 or 32768 entries: the paper's 2-bit
+ * configurations, appendix "Experimental Configurations"; 15-bit codes are
+ * stored one per uint16).  Sizes: d_out * (d_in / g) must stay below 2^31
+ * and d_out, d_in, n below 2^31.
  *
  * Alignment: codes, codebooks, x, y and w_out must be 16-byte aligned and
- * scales 2-byte aligned.  Shapes whose code row pitch (d_in/g * M * B/8 bytes)
- * is a multiple of 16 take the vectorized load path; any other shape takes a
- * slower generic path with the same results.
+ * scales 2-byte aligned.  Shapes whose code row pitch (d_in/g * M bytes for
+ * 8-bit codes, twice that for 15- and 16-bit codes) is a multiple of 16 take
+ * the vectorized load path; any other shape takes a slower generic path with
+ * the same results.
  *
  * Errors: all argument checks run on the host before anything is launched; on
  * an error nothing is launched and no output is touched.  A HIP launch error

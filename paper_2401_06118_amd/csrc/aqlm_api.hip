@@ -54,7 +54,7 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
   if (!codes || !codebooks || !scales) return AQLM_ERR_NULL;
   if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return AQLM_ERR_SHAPE;
   if (g != 8) return AQLM_ERR_UNSUPPORTED;
-  if (!((B == 8 && M >= 1 && M <= 8) || (B == 16 && M == 1))) return AQLM_ERR_UNSUPPORTED;
+  if (!((B == 8 && M >= 1 && M <= 8) || ((B == 15 || B == 16) && M == 1))) return AQLM_ERR_UNSUPPORTED;
   const int64_t G = d_in / g;
   // (sizes and offsets are held in 32 bits on the device side)
   if (d_out >= (int64_t(1) << 31) || d_in >= (int64_t(1) << 31) || d_out * G >= (int64_t(1) << 31))
@@ -68,7 +68,7 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
   L->G = (int32_t)G;
   L->M = M;
   L->B = B;
-  const int64_t pitch = G * M * (B / 8);
+  const int64_t pitch = G * M * (B > 8 ? 2 : 1);
   L->vec_codes = (pitch % 16) == 0;
   return AQLM_OK;
 }
@@ -149,7 +149,7 @@ int gemm_dispatch(const aqlm::Layer& L, int64_t n, const uint16_t* x, uint16_t* 
   // scheme with one MFMA column per token; otherwise the tiled kernel.
   if (aqlm::gemm_nb_supported(L, (int32_t)n)) return status_of(aqlm::launch_gemm_nb(L, (int32_t)n, x, y, s));
   const bool chunk_nb = n <= kChunkedMax && aqlm::gemm_nb_supported(L, (int32_t)kSmallBatchMax);
-  const bool chunk_16 = n <= kChunkedMax16 && L.B == 16 && aqlm::mfma_supported(L);
+  const bool chunk_16 = n <= kChunkedMax16 && L.B > 8 && aqlm::mfma_supported(L);
   if (n > kSmallBatchMax && (chunk_nb || chunk_16)) {
     for (int64_t t0 = 0; t0 < n; t0 += kSmallBatchMax) {
       const int64_t nt = n - t0 < kSmallBatchMax ? n - t0 : kSmallBatchMax;

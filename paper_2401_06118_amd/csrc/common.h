@@ -22,6 +22,11 @@ struct IntC {
   static constexpr int value = V;
 };
 
+// Code storage: B <= 8 in one byte, 8 < B <= 16 in two (unpacked); a code
+// is masked to its B bits before it indexes a codebook of 2^B codewords.
+constexpr int code_bytes(int B) { return B > 8 ? 2 : 1; }
+constexpr uint32_t code_mask(int B) { return (1u << B) - 1u; }
+
 __device__ __forceinline__ float h2f(uint16_t h) { return (float)__builtin_bit_cast(_Float16, h); }
 // Round to fp16 with the hardware conversion (round to nearest even under the
 // default MODE; fp16 subnormals are kept).

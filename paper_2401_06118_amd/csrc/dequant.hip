@@ -14,8 +14,8 @@ namespace aqlm {
 
 template <int M, int B>
 __device__ __forceinline__ void load_group_codes(const void* __restrict__ codes, uint32_t q, uint32_t (&c)[M]) {
-  if constexpr (B == 16) {
-    c[0] = static_cast<const uint16_t*>(codes)[q];
+  if constexpr (B > 8) {
+    c[0] = static_cast<const uint16_t*>(codes)[q] & code_mask(B);
   } else {
     const uint8_t* p = static_cast<const uint8_t*>(codes) + (size_t)q * M;
     if constexpr (M == 2) {
@@ -101,6 +101,7 @@ static hipError_t run_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
 
 hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
   if (L.B == 16) return run_dequant<1, 16>(L, w, s);
+  if (L.B == 15) return run_dequant<1, 15>(L, w, s);
   switch (L.M) {
     case 1: return run_dequant<1, 8>(L, w, s);
     case 2: return run_dequant<2, 8>(L, w, s);

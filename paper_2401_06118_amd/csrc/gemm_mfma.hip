@@ -30,9 +30,9 @@ constexpr int kQT = 4 * kCPL;    // codes per row per K-tile
 
 template <int M, int B>
 struct MfmaCfg {
-  static constexpr int kBytesPerCode = B / 8;
+  static constexpr int kBytesPerCode = code_bytes(B);
   static constexpr int kGT = kQT / M;  // groups (x-slices) per K-tile
-  static constexpr int kCopies = (B == 16) ? 0 : (M <= 2 ? 16 : (M <= 4 ? 8 : 4));
+  static constexpr int kCopies = (B > 8) ? 0 : (M <= 2 ? 16 : (M <= 4 ? 8 : 4));
   static constexpr int kLaneBytes = kCPL * kBytesPerCode;  // 8 or 16
   static constexpr int kWords = kLaneBytes / 4;
 };
@@ -67,7 +67,7 @@ __device__ __forceinline__ void load_codes8(const uint8_t* __restrict__ codes, i
 
 template <int B>
 __device__ __forceinline__ uint32_t code_k(const uint32_t* w, int k) {
-  if constexpr (B == 16) return (w[k / 2] >> (16 * (k % 2))) & 0xFFFFu;
+  if constexpr (B > 8) return (w[k / 2] >> (16 * (k % 2))) & code_mask(B);
   return (w[k / 4] >> (8 * (k % 4))) & 0xFFu;
 }
 
@@ -259,12 +259,13 @@ hipError_t run_vec(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hi
 }  // namespace
 
 bool mfma_supported(const Layer& L) {
-  if (L.B == 16) return L.M == 1;
+  if (L.B > 8) return L.M == 1;
   return L.M == 1 || L.M == 2 || L.M == 4 || L.M == 8;
 }
 
 hipError_t launch_gemm_mfma(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s) {
   if (L.B == 16) return run_vec<1, 16>(L, n, x, y, s);
+  if (L.B == 15) return run_vec<1, 15>(L, n, x, y, s);
   switch (L.M) {
     case 1: return run_vec<1, 8>(L, n, x, y, s);
     case 2: return run_vec<2, 8>(L, n, x, y, s);

@@ -26,11 +26,11 @@ constexpr int kMaxPartials = 2048;
 
 template <int M, int B>
 struct GemvCfg {
-  static constexpr int kBytesPerCode = B / 8;
+  static constexpr int kBytesPerCode = code_bytes(B);
   static constexpr int GPL = (M * kBytesPerCode <= 2) ? 8 : (M * kBytesPerCode <= 4 ? 4 : 2);
   static constexpr int kCodeBytes = GPL * M * kBytesPerCode;  // per lane per item
   static constexpr int kWords = (kCodeBytes + 3) / 4;
-  static constexpr int kCopies = (B == 16) ? 0 : (M <= 2 ? 16 : (M <= 4 ? 8 : 4));
+  static constexpr int kCopies = (B > 8) ? 0 : (M <= 2 ? 16 : (M <= 4 ? 8 : 4));
   static constexpr int kChunkGroups = 64 * GPL;
   static constexpr bool kCanVec = (kCodeBytes == 16 || kCodeBytes == 8);
 };
@@ -70,9 +70,9 @@ __device__ __forceinline__ void load_lane_codes(const uint8_t* __restrict__ code
 
 template <int M, int B>
 __device__ __forceinline__ uint32_t code_at(const uint32_t* w, int gi, int m) {
-  if constexpr (B == 16) {
+  if constexpr (B > 8) {
     const int k = gi * M + m;
-    return (w[k / 2] >> (16 * (k % 2))) & 0xFFFFu;
+    return (w[k / 2] >> (16 * (k % 2))) & code_mask(B);
   } else {
     const int b = gi * M + m;
     return (w[b / 4] >> (8 * (b % 4))) & 0xFFu;
@@ -210,6 +210,7 @@ static hipError_t run_gemv_v(const Layer& L, const uint16_t* x, uint16_t* y, hip
 
 hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s) {
   if (L.B == 16) return run_gemv_v<1, 16>(L, x, y, s);
+  if (L.B == 15) return run_gemv_v<1, 15>(L, x, y, s);
   switch (L.M) {
     case 1: return run_gemv_v<1, 8>(L, x, y, s);
     case 2: return run_gemv_v<2, 8>(L, x, y, s);

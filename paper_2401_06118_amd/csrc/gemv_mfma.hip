@@ -164,14 +164,14 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
       const int k = k0 + u;
       const uint32_t cw[4] = {buf[u][0], buf[u][1], buf[u][2], buf[u][3]};
       uint4 av[C::kCPL];
-      if constexpr (B == 16) {
+      if constexpr (B > 8) {
         // L2 gathers go out before the next code load so that waiting for
         // them does not wait for HBM.
         if (k < nk) {
 #pragma unroll
           for (int t = 0; t < C::kCPL; ++t)
             av[t] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb) +
-                                                     (((cw[t / 2] >> (16 * (t % 2))) & 0xFFFFu) << 4));
+                                                     (((cw[t / 2] >> (16 * (t % 2))) & code_mask(B)) << 4));
         }
       }
       issue(f_rb, f_ks, buf[u]);
@@ -468,7 +468,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
 // registers for all passes.  The next chunk is loaded into registers while the
 // current one is in use, then written to LDS between passes.
 constexpr int kCbChunk = 8192;                  // codewords per LDS chunk
-constexpr int kCbPasses = 65536 / kCbChunk;     // chunks of a 16-bit codebook
+constexpr int cb_passes(int B) { return (1 << B) / kCbChunk; }  // chunks of a 2^B codebook (B >= 13)
 constexpr int kCbStage = kCbChunk / kThreads;   // 16-byte chunk loads per thread
 
 // LDS byte addresses of the two codewords of a 32-bit code word in the chunk
@@ -476,9 +476,11 @@ constexpr int kCbStage = kCbChunk / kThreads;   // 16-byte chunk loads per threa
 // chunk gives the zero codeword at entry kCbChunk.  Packed 16-bit arithmetic
 // wraps modulo 2^16, so (code - first) lands in [0, kCbChunk) exactly for the
 // codes of the chunk and above it otherwise.
+template <int B>
 __device__ __forceinline__ void cb_chunk_addr(uint32_t word, uint32_t first2, uint32_t base, uint32_t& a0,
                                               uint32_t& a1) {
   typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
+  if constexpr (B < 16) word &= code_mask(B) * 0x10001u;
   u16x2_t t = __builtin_bit_cast(u16x2_t, word) - __builtin_bit_cast(u16x2_t, first2);
   t = __builtin_elementwise_min(t, (u16x2_t){(uint16_t)kCbChunk, (uint16_t)kCbChunk});
   const uint32_t tw = __builtin_bit_cast(uint32_t, t);
@@ -488,8 +490,10 @@ __device__ __forceinline__ void cb_chunk_addr(uint32_t word, uint32_t first2, ui
   asm("v_mad_u32_u16 %0, %1, 16, %2 op_sel:[1,0,0,0]" : "=v"(a1) : "v"(tw), "v"(base));
 }
 
-template <int NKS, int RB>
+template <int NKS, int RB, int B>
 __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
+  constexpr int kCbPasses = cb_passes(B);
+  static_assert(kCbPasses * kCbChunk == (1 << B), "whole chunks");
   constexpr int kItems = NKS * RB;
   constexpr int kXG = NKS * kWaves * 32;        // x groups staged (K-slices of 32 groups), zero past G
   constexpr int kXL = (kXG + kThreads - 1) / kThreads;
@@ -597,11 +601,11 @@ __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
           for (int u = 0; u < kStep; u += 2) {
             const int t = t0 + u;
             uint32_t a0, a1;
-            cb_chunk_addr(cw[j * RB + rb][t / 2], first2, base, a0, a1);
+            cb_chunk_addr<B>(cw[j * RB + rb][t / 2], first2, base, a0, a1);
             av[u] = lds_load16(a0);
             av[u + 1] = lds_load16(a1);
             if (pair) {
-              cb_chunk_addr(cw[j * RB + (pair ? rb + 1 : rb)][t / 2], first2, base, a0, a1);
+              cb_chunk_addr<B>(cw[j * RB + (pair ? rb + 1 : rb)][t / 2], first2, base, a0, a1);
               bv[u] = lds_load16(a0);
               bv[u + 1] = lds_load16(a1);
             }
@@ -651,9 +655,9 @@ __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
   }
 }
 
-template <int NKS, int RB>
+template <int NKS, int RB, int B>
 hipError_t launch_cb(const GemvBatch& bt, hipStream_t s) {
-  auto kern = k_gemv_cb<NKS, RB>;
+  auto kern = k_gemv_cb<NKS, RB, B>;
   {
     const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), 160 * 1024);
     if (e != hipSuccess) return e;
@@ -669,20 +673,21 @@ hipError_t launch_cb(const GemvBatch& bt, hipStream_t s) {
 constexpr int kCbMaxNks = 3;
 constexpr int cb_rb_cap(int nks) { return nks == 1 ? 6 : (nks == 2 ? 4 : 2); }
 
+template <int B>
 hipError_t launch_cb_shape(const GemvBatch& bt, int nks, int rb, hipStream_t s) {
   switch (nks * 8 + rb) {
-    case 8 + 1: return launch_cb<1, 1>(bt, s);
-    case 8 + 2: return launch_cb<1, 2>(bt, s);
-    case 8 + 3: return launch_cb<1, 3>(bt, s);
-    case 8 + 4: return launch_cb<1, 4>(bt, s);
-    case 8 + 5: return launch_cb<1, 5>(bt, s);
-    case 8 + 6: return launch_cb<1, 6>(bt, s);
-    case 16 + 1: return launch_cb<2, 1>(bt, s);
-    case 16 + 2: return launch_cb<2, 2>(bt, s);
-    case 16 + 3: return launch_cb<2, 3>(bt, s);
-    case 16 + 4: return launch_cb<2, 4>(bt, s);
-    case 24 + 1: return launch_cb<3, 1>(bt, s);
-    case 24 + 2: return launch_cb<3, 2>(bt, s);
+    case 8 + 1: return launch_cb<1, 1, B>(bt, s);
+    case 8 + 2: return launch_cb<1, 2, B>(bt, s);
+    case 8 + 3: return launch_cb<1, 3, B>(bt, s);
+    case 8 + 4: return launch_cb<1, 4, B>(bt, s);
+    case 8 + 5: return launch_cb<1, 5, B>(bt, s);
+    case 8 + 6: return launch_cb<1, 6, B>(bt, s);
+    case 16 + 1: return launch_cb<2, 1, B>(bt, s);
+    case 16 + 2: return launch_cb<2, 2, B>(bt, s);
+    case 16 + 3: return launch_cb<2, 3, B>(bt, s);
+    case 16 + 4: return launch_cb<2, 4, B>(bt, s);
+    case 24 + 1: return launch_cb<3, 1, B>(bt, s);
+    case 24 + 2: return launch_cb<3, 2, B>(bt, s);
   }
   return hipErrorInvalidValue;
 }
@@ -763,7 +768,9 @@ hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStrea
 
 }  // namespace
 
-bool gemv_mfma_supported(int M, int B) { return (B == 16 && M == 1) || (B == 8 && (M == 1 || M == 2 || M == 4)); }
+bool gemv_mfma_supported(int M, int B) {
+  return ((B == 15 || B == 16) && M == 1) || (B == 8 && (M == 1 || M == 2 || M == 4));
+}
 
 // Whether x (staged whole in LDS, at most kXL groups per thread) and the
 // partial sums fit, next to at least one codebook copy for 8-bit codes.
@@ -771,7 +778,7 @@ bool gemv_mfma_fits(const Layer* Ls, int count) {
   for (int i = 0; i < count; ++i) {
     const Layer& L = Ls[i];
     const int kCPL = (L.B == 8) ? 16 : 8, kKS = 4 * kCPL, xl = (L.B == 8) ? 4 : 8;
-    const int64_t KS = ((int64_t)L.G * L.M * (L.B / 8) + 63) / 64;
+    const int64_t KS = ((int64_t)L.G * L.M * code_bytes(L.B) + 63) / 64;
     const int64_t xg = KS * (kKS / L.M);
     if (xg > (int64_t)xl * kThreads) return false;
     const size_t need = (size_t)xg * 16 + (size_t)kMaxRB * kWaves * 16 * 4 + (L.B == 8 ? (size_t)L.M * 256 * 16 : 0);
@@ -792,13 +799,13 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   double total_bytes = 0;
   for (int i = 0; i < count; ++i) {
     vec = vec && Ls[i].vec_codes;
-    total_bytes += (double)Ls[i].d_out * Ls[i].G * M * (B / 8);
+    total_bytes += (double)Ls[i].d_out * Ls[i].G * M * code_bytes(B);
   }
   const int cus = num_cus();
   // 1x16 runs the chunked-codebook kernel where its code items fit in
   // registers and x next to the chunk (NKS K-slices per wave).
   int cb_nks = 0;
-  if (B == 16 && vec) {
+  if (B > 8 && vec) {
     for (int i = 0; i < count; ++i) {
       const int KS = (int)(((int64_t)Ls[i].G * 2 + 63) / 64);
       const int nks = (KS + kWaves - 1) / kWaves;
@@ -820,7 +827,7 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     double rem[kMaxProblems];
     int sum = 0;
     for (int i = 0; i < count; ++i) {
-      const double share = cus * ((double)Ls[i].d_out * Ls[i].G * M * (B / 8)) / total_bytes;
+      const double share = cus * ((double)Ls[i].d_out * Ls[i].G * M * code_bytes(B)) / total_bytes;
       want_of[i] = share < 1.0 ? 1 : (int)share;
       rem[i] = share - (double)want_of[i];
       sum += want_of[i];
@@ -855,7 +862,7 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     // At most rb_cap row blocks per workgroup (accumulator registers and
     // partial-sum space).  Larger layers run `rounds` workgroups per CU,
     // split evenly rather than leaving a short last round.
-    const int rb_cap = (B == 16) ? (cb_nks > 0 ? cb_rb_cap(cb_nks) : kMaxRB) : ks_rb_cap(M);
+    const int rb_cap = (B > 8) ? (cb_nks > 0 ? cb_rb_cap(cb_nks) : kMaxRB) : ks_rb_cap(M);
     const int blocks = (L.d_out + 15) / 16;
     const int rounds = (blocks + rb_cap * want - 1) / (rb_cap * want);
     const int rows_per_wg = (L.d_out + want * rounds - 1) / (want * rounds);
@@ -887,9 +894,12 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   if (xg_max > xl * kThreads) return hipErrorInvalidValue;
   const size_t base = (size_t)xg_max * 16 + (size_t)rb_max * kWaves * 16 * 4;
   const size_t limit = 160 * 1024;
-  if (B == 16 && cb_nks > 0) return launch_cb_shape(bt, cb_nks, rb_max, s);
-  if (B == 16) {
+  if (B > 8 && cb_nks > 0)
+    return B == 15 ? launch_cb_shape<15>(bt, cb_nks, rb_max, s) : launch_cb_shape<16>(bt, cb_nks, rb_max, s);
+  if (B > 8) {
     if (base > limit) return hipErrorInvalidValue;
+    if (B == 15)
+      return vec ? launch_copies<1, 15, 0, true>(bt, ni, base, s) : launch_copies<1, 15, 0, false>(bt, ni, base, s);
     return vec ? launch_copies<1, 16, 0, true>(bt, ni, base, s) : launch_copies<1, 16, 0, false>(bt, ni, base, s);
   }
   // the most codebook copies that fit next to x and the partials

@@ -49,18 +49,18 @@ template <int M, int B, int BN>
 struct PfCfg {
   static constexpr int kXTileU4 = BN * kPitchU4;
   static constexpr int kTB = BN / 32;  // 16-token blocks per consumer wave = x rows per producer thread
-  static constexpr int kBpc = B / 8;
+  static constexpr int kBpc = code_bytes(B);
   static constexpr int kCodeBytes = 4 * M * kBpc;  // codes of a producer thread's 4 groups
   static constexpr int kCodeWords = (kCodeBytes + 3) / 4;
   // 32 KiB of codebook copies: the tiles take the rest of the LDS
-  static constexpr int kCopies = (B == 16) ? 0 : 8 / M;
-  static constexpr size_t kCbBytes = (B == 16) ? 0 : (size_t)M * 256 * 16 * kCopies;
+  static constexpr int kCopies = (B > 8) ? 0 : 8 / M;
+  static constexpr size_t kCbBytes = (B > 8) ? 0 : (size_t)M * 256 * 16 * kCopies;
   static constexpr size_t kLds = kCbBytes + 2 * (size_t)(kATileU4 + kXTileU4) * 16;
 };
 
 template <int B>
 __device__ __forceinline__ uint32_t code_at(const uint32_t* w, int q) {
-  if constexpr (B == 16) return (w[q / 2] >> (16 * (q % 2))) & 0xFFFFu;
+  if constexpr (B > 8) return (w[q / 2] >> (16 * (q % 2))) & code_mask(B);
   return (w[q / 4] >> (8 * (q % 4))) & 0xFFu;
 }
 
@@ -213,16 +213,16 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
     // only stores and barriers depend on the step count.
     auto p_step = [&](int k, auto set_next, auto set_after) {  // while step k is multiplied
       if (k + 1 < ksteps) p_store(k + 1, set_next);
-      if constexpr (B == 16) p_gather(set_after);
+      if constexpr (B > 8) p_gather(set_after);
       p_load(k + 3, set_next);
     };
     p_load(0, IntC<0>{});
     p_load(1, IntC<1>{});
     __syncthreads();  // codebook copies visible
-    if constexpr (B == 16) p_gather(IntC<0>{});
+    if constexpr (B > 8) p_gather(IntC<0>{});
     p_store(0, IntC<0>{});
     p_load(2, IntC<0>{});
-    if constexpr (B == 16) p_gather(IntC<1>{});
+    if constexpr (B > 8) p_gather(IntC<1>{});
     __syncthreads();
     for (int k = 0; k < ksteps; k += 2) {
       p_step(k, IntC<1>{}, IntC<0>{});
@@ -285,7 +285,7 @@ hipError_t run_prefill_bn(const Layer& L, int32_t n, const uint16_t* x, uint16_t
   using P = PfCfg<M, B, BN>;
   static_assert(P::kLds <= kPfLdsLimit, "prefill LDS budget");
   // 8-byte / 16-byte code loads need every row's code pitch to keep that alignment
-  const bool vec = ((int64_t)L.G * M * (B / 8)) % P::kCodeBytes == 0;
+  const bool vec = ((int64_t)L.G * M * code_bytes(B)) % P::kCodeBytes == 0;
   auto kern = vec ? k_prefill<M, B, BN, true> : k_prefill<M, B, BN, false>;
   {
     const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), (int)kPfLdsLimit);
@@ -319,12 +319,13 @@ hipError_t run_prefill(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y
 }  // namespace
 
 bool prefill_supported(const Layer& L) {
-  if (L.B == 16) return L.M == 1;
+  if (L.B > 8) return L.M == 1;
   return L.M == 1 || L.M == 2 || L.M == 4;
 }
 
 hipError_t launch_prefill(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s) {
   if (L.B == 16) return L.M == 1 ? run_prefill<1, 16>(L, n, x, y, s) : hipErrorInvalidValue;
+  if (L.B == 15) return L.M == 1 ? run_prefill<1, 15>(L, n, x, y, s) : hipErrorInvalidValue;
   switch (L.M) {
     case 1: return run_prefill<1, 8>(L, n, x, y, s);
     case 2: return run_prefill<2, 8>(L, n, x, y, s);

@@ -9,7 +9,7 @@ namespace aqlm {
 
 template <int B>
 struct GCfg {
-  static constexpr int kBpc = B / 8;          // bytes per code
+  static constexpr int kBpc = code_bytes(B);  // bytes per code
   static constexpr int kCPL = 16 / kBpc;      // codes per lane per item
   static constexpr int kKS = 4 * kCPL;        // codes per row per item
   static constexpr int kXL = (B == 8) ? 4 : 8;  // x staging loads per thread (groups <= kXL * 1024)

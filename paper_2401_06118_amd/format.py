@@ -38,7 +38,8 @@ class AqlmShape:
         return self.storage_bits() / (self.d_out * self.d_in)
 
     def codes_bytes(self) -> int:
-        """Bytes of the code tensor as the library stores it (B in {8, 16}: no padding)."""
+        """Bytes of the code tensor as the library stores it: one byte per code for
+        B <= 8, two for 8 < B <= 16 (unpacked, no padding)."""
         return self.d_out * self.groups * self.code_bytes_per_group
 
     def codebook_bytes(self) -> int:

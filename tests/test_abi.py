@@ -95,7 +95,9 @@ def test_unsupported_formats(lib, fn):
     assert fn(lib, M=0) == UNSUP
     assert fn(lib, M=9) == UNSUP
     assert fn(lib, M=2, B=16) == UNSUP
+    assert fn(lib, M=2, B=15) == UNSUP
     assert fn(lib, M=1, B=12) == UNSUP
+    assert fn(lib, M=1, B=14) == UNSUP
     assert fn(lib, M=1, B=4) == UNSUP
 
 

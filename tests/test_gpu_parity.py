@@ -484,3 +484,58 @@ def test_gemm_random_shapes(seed):
     torch.cuda.synchronize()
     check_products(lay, fp16_to_np(y1))
     check_products(lay, fp16_to_np(y2))
+
+
+# -------------------------------------------------- 1x15 (15-bit codes)
+
+@pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (11008, 4096), (4096, 11008), (1000, 4104), (37, 8)])
+def test_1x15_gemv_matches_oracle(d_out, d_in):
+    """One codebook of 2^15 codewords, codes stored as uint16 (the unpacked
+    reading): the L2-gather and the chunked kernels (four chunks), aligned
+    and unaligned code rows."""
+    print(f"[1x15 gemv] {d_out}x{d_in}", flush=True)
+    lay = synth.layer(16_000 + d_out + d_in, d_out, d_in, 1, 15)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemv(codes, cb, sc, x[0])
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y)[None, :])
+
+
+def test_1x15_grouped_matches_oracle():
+    _grouped_case([(4096, 4096)] * 3, 1, 15, 16_100)
+    _grouped_case([(11008, 4096)] * 2, 1, 15, 16_200)
+
+
+@pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (1000, 4104)])
+def test_1x15_dequantize_bit_exact(d_out, d_in):
+    lay = synth.layer(16_300 + d_out, d_out, d_in, 1, 15)
+    assert_bits_equal(dequant_gpu(lay), oracle.dequantize(lay.codes, lay.codebooks, lay.scales))
+
+
+@pytest.mark.parametrize("n", [4, 16, 32, 100, 300])
+def test_1x15_gemm_matches_oracle(n):
+    """Small batch (chunks of 16), the tiled and prefill kernels, and the
+    workspace path."""
+    print(f"[1x15 gemm] n={n}", flush=True)
+    lay = synth.layer(16_400 + n, 1100, 2048, 1, 15, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y1 = aq().gemm_small_batch(codes, cb, sc, x)
+    y2 = aq().gemm(codes, cb, sc, x)
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y1))
+    check_products(lay, fp16_to_np(y2))
+
+
+def test_1x15_high_code_bits_are_ignored():
+    """Codes are taken modulo 2^15: setting bit 15 of every code changes
+    nothing (no codeword outside the 2^15-entry codebook is read)."""
+    lay = synth.layer(16_500, 512, 1024, 1, 15)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemv(codes, cb, sc, x[0])
+    w = aq().dequantize(codes, cb, sc)
+    high = (codes.view(torch.int16) | torch.tensor(-32768, dtype=torch.int16, device="cuda")).contiguous()
+    y_hi = aq().gemv(high, cb, sc, x[0])
+    w_hi = aq().dequantize(high, cb, sc)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y_hi.view(torch.int16))
+    assert torch.equal(w.view(torch.int16), w_hi.view(torch.int16))
