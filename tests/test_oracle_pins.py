@@ -98,14 +98,19 @@ def brute_force_dequant(codes, codebooks, scales):
     d_out, groups, M = codes.shape
     _, entries, g = codebooks.shape
     C = [codebooks[m].astype(np.float32).T for m in range(M)]  # g x 2^B
-    eye = np.eye(entries, dtype=np.float32)
+
+    def one_hot(c):
+        v = np.zeros(entries, dtype=np.float32)
+        v[c] = 1.0
+        return v
+
     rows = []
     for i in range(d_out):
         parts = []
         for j in range(groups):
-            acc = C[0] @ eye[codes[i, j, 0]]
+            acc = C[0] @ one_hot(codes[i, j, 0])
             for m in range(1, M):
-                acc = (acc + C[m] @ eye[codes[i, j, m]]).astype(np.float32)
+                acc = (acc + C[m] @ one_hot(codes[i, j, m])).astype(np.float32)
             parts.append(acc)
         row = np.concatenate(parts).astype(np.float32) * np.float32(scales[i])
         with np.errstate(over="ignore"):
@@ -113,13 +118,16 @@ def brute_force_dequant(codes, codebooks, scales):
     return np.stack(rows)
 
 
-@pytest.mark.parametrize("M,B,g", [(1, 2, 8), (2, 2, 8), (3, 3, 4), (4, 4, 2), (2, 4, 8), (1, 4, 1)])
+@pytest.mark.parametrize("M,B,g", [(1, 2, 8), (2, 2, 8), (3, 3, 4), (4, 4, 2), (2, 4, 8), (1, 4, 1),
+                                   (2, 12, 8), (2, 15, 8), (2, 16, 8)])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_dequant_matches_one_hot_brute_force(M, B, g, seed):
+    """Includes two codebooks of 12-, 15- and 16-bit codes (the 3- and 4-bit
+    settings of App. "Experimental Configurations"), stored as uint16."""
     rng = np.random.default_rng(100 * seed + 10 * M + B)
     d_out, groups = int(rng.integers(1, 9)), int(rng.integers(1, 5))
     codebooks = rng.standard_normal((M, 1 << B, g)).astype(np.float16)
-    codes = rng.integers(0, 1 << B, size=(d_out, groups, M), dtype=np.uint8)
+    codes = rng.integers(0, 1 << B, size=(d_out, groups, M), dtype=np.uint8 if B <= 8 else np.uint16)
     scales = rng.uniform(-2, 2, size=d_out).astype(np.float16)
     w = oracle.dequantize(codes, codebooks, scales, g).view(np.float16)
     ref = brute_force_dequant(codes, codebooks, scales)
@@ -195,19 +203,22 @@ def test_identity_codebook_reproduces_plain_fp16_matvec():
     assert np.all(np.abs(y - exact) <= bound)
 
 
-@pytest.mark.parametrize("M", [1, 2])
-def test_unit_vector_codebook_closed_form(M):
+@pytest.mark.parametrize("M,B", [(1, 8), (2, 8), (2, 12), (2, 16)])
+def test_unit_vector_codebook_closed_form(M, B):
     """C_0[k] = e_(k mod 8); with M=2 also C_1[k] = 2 e_((k div 8) mod 8).  Then
     W[i, 8j + t] = s_i (1[t = a mod 8] + 2 * 1[t = (b div 8) mod 8]) and
-    y_i = s_i * sum_j (x[8j + a mod 8] + 2 x[8j + (b div 8) mod 8])."""
-    rng = np.random.default_rng(21 + M)
-    d_out, d_in, B = 64, 96, 8
-    cb = np.zeros((M, 256, 8), dtype=np.float16)
-    k = np.arange(256)
+    y_i = s_i * sum_j (x[8j + a mod 8] + 2 x[8j + (b div 8) mod 8]).  With
+    wide codes, reading the second codebook at the first one's offset breaks
+    the closed form (the brute-force pin covers cut-off code bits)."""
+    rng = np.random.default_rng(21 + M + B)
+    d_out, d_in = 64, 96
+    entries = 1 << B
+    cb = np.zeros((M, entries, 8), dtype=np.float16)
+    k = np.arange(entries)
     cb[0, k, k % 8] = 1.0
     if M == 2:
         cb[1, k, (k // 8) % 8] = 2.0
-    codes = rng.integers(0, 256, size=(d_out, d_in // 8, M), dtype=np.uint8)
+    codes = rng.integers(0, entries, size=(d_out, d_in // 8, M), dtype=np.uint8 if B <= 8 else np.uint16)
     scales = rng.choice(np.array([0.5, 1.0, 1.5, 0.75], np.float16), size=d_out)
     x = rng.standard_normal((1, d_in)).astype(np.float16)
     y = oracle.aqlm_matmul(codes, cb, scales, x)[0]
