@@ -283,6 +283,8 @@ def single_layer_rows(aq, torch):
         "4096x11008 1x16": (4096, 11008, 1, 16),
         "4096x4096 1x15": (4096, 4096, 1, 15),
         "11008x4096 1x15": (11008, 4096, 1, 15),
+        "11008x4096 2x12": (11008, 4096, 2, 12),
+        "11008x4096 2x16": (11008, 4096, 2, 16),
         "28672x8192 2x8": (28672, 8192, 2, 8),
     }.items():
         from paper_2401_06118_amd import format as fmt
@@ -432,7 +434,7 @@ def main():
         "dtype": "f16 (fp32 accumulate)",
         "data": "synthetic: uniform codes, N(0,0.02) fp16 codebooks, U[0.5,1.5] fp16 scales, N(0,1) fp16 x",
         "config": {
-            "workload": f"Llama-2-{model.upper()} decode step, linear layers only, AQLM {M}x{B if B == 16 else 8} "
+            "workload": f"Llama-2-{model.upper()} decode step, linear layers only, AQLM {M}x{B} "
                         f"g8, batch 1: {len(layers)} GEMVs in {len(launches)} launches (per block: grouped "
                         f"q/k/v, o, grouped gate/up, down), replayed as one HIP graph",
             "layers": len(layers),

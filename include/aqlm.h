@@ -20,7 +20,7 @@
  *
  * Layouts (dense, row-major, contiguous):
  *   codes      [d_out][d_in/g][M], m fastest.  uint8_t when B = 8,
- *              uint16_t when B = 15 or 16 (unpacked); value = codeword
+ *              uint16_t when B = 12, 15 or 16 (unpacked); value = codeword
  *              index, taken modulo 2^B.
  *   codebooks  [M][2^B][g] fp16 (one codeword = g contiguous values).
  *   scales     [d_out] fp16.
@@ -28,16 +28,19 @@
  *   y          [n][d_out] fp16.
  *   w_out      [d_out][d_in] fp16.
  *
- * Supported formats: g = 8 and either B = 8 with 1 <= M <= 8 (M codebooks of
- * 256 entries, e.g. the paper's 2x8 and 4x8 schemes) or B = 16 or 15 with
- * M = 1 (one codebook of 65536 or 32768 entries: the paper's 2-bit
- * configurations, appendix "Experimental Configurations"; 15-bit codes are
- * stored one per uint16).  Sizes: d_out * (d_in / g) must stay below 2^31
- * and d_out, d_in, n below 2^31.
+ * Supported formats, all with g = 8 (the 2x8 model of Sec. 4.3 and the 2-,
+ * 3- and 4-bit settings of the appendix "Experimental Configurations"):
+ *   B = 8,  1 <= M <= 8   M codebooks of 256 entries;
+ *   B = 15 or 16, M = 1   one codebook of 32768 or 65536 entries (2 bits);
+ *   B = 12, M = 2         two codebooks of 4096 entries (3 bits);
+ *   B = 15 or 16, M = 2   two codebooks of 32768 or 65536 entries (4 bits).
+ * Codes wider than 8 bits are stored one per uint16, without bit packing.
+ * Sizes: d_out * (d_in / g) must stay below 2^31 and d_out, d_in, n below
+ * 2^31.
  *
  * Alignment: codes, codebooks, x, y and w_out must be 16-byte aligned and
  * scales 2-byte aligned.  Shapes whose code row pitch (d_in/g * M bytes for
- * 8-bit codes, twice that for 15- and 16-bit codes) is a multiple of 16 take
+ * 8-bit codes, twice that for wider codes) is a multiple of 16 take
  * the vectorized load path; any other shape takes a slower generic path with
  * the same results.
  *

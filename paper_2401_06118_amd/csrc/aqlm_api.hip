@@ -54,7 +54,7 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
   if (!codes || !codebooks || !scales) return AQLM_ERR_NULL;
   if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return AQLM_ERR_SHAPE;
   if (g != 8) return AQLM_ERR_UNSUPPORTED;
-  if (!((B == 8 && M >= 1 && M <= 8) || ((B == 15 || B == 16) && M == 1))) return AQLM_ERR_UNSUPPORTED;
+  if (!aqlm::format_supported(M, B)) return AQLM_ERR_UNSUPPORTED;
   const int64_t G = d_in / g;
   // (sizes and offsets are held in 32 bits on the device side)
   if (d_out >= (int64_t(1) << 31) || d_in >= (int64_t(1) << 31) || d_out * G >= (int64_t(1) << 31))

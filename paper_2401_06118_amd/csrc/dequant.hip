@@ -5,8 +5,8 @@
 // Each thread writes one group of 8 weights (16 bytes); consecutive threads
 // write consecutive groups, so both the code reads and the fp16 writes are
 // fully coalesced.  The kernel is bound by the 16-byte-per-group write
-// stream.  For B = 8 the M codebooks (4 KiB each) sit in LDS; for B = 16 the
-// 1 MiB codebook is read through L2.
+// stream.  For B = 8 the M codebooks (4 KiB each) sit in LDS; wider codes
+// read their codebooks (up to 2 x 1 MiB) through L2.
 #include "common.h"
 #include "launch.h"
 
@@ -15,7 +15,14 @@ namespace aqlm {
 template <int M, int B>
 __device__ __forceinline__ void load_group_codes(const void* __restrict__ codes, uint32_t q, uint32_t (&c)[M]) {
   if constexpr (B > 8) {
-    c[0] = static_cast<const uint16_t*>(codes)[q] & code_mask(B);
+    const uint16_t* p = static_cast<const uint16_t*>(codes) + (size_t)q * M;
+    if constexpr (M == 2) {
+      const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
+      c[0] = v & code_mask(B);
+      c[1] = (v >> 16) & code_mask(B);
+    } else {
+      c[0] = p[0] & code_mask(B);
+    }
   } else {
     const uint8_t* p = static_cast<const uint8_t*>(codes) + (size_t)q * M;
     if constexpr (M == 2) {
@@ -69,7 +76,7 @@ __global__ __launch_bounds__(256) void k_dequant(const void* __restrict__ codes,
 #pragma unroll
     for (int m = 1; m < M; ++m) {
       float v[8];
-      unpack8(cb_lds[m * 256 + c[m]], v);
+      unpack8((B == 8) ? cb_lds[m * 256 + c[m]] : cb[((uint32_t)m << B) + c[m]], v);
 #pragma unroll
       for (int k = 0; k < 8; ++k) acc[k] = acc[k] + v[k];
     }
@@ -100,8 +107,15 @@ static hipError_t run_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
 }
 
 hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
-  if (L.B == 16) return run_dequant<1, 16>(L, w, s);
-  if (L.B == 15) return run_dequant<1, 15>(L, w, s);
+  if (L.B > 8) {
+    if (L.M == 1) return L.B == 16 ? run_dequant<1, 16>(L, w, s) : run_dequant<1, 15>(L, w, s);
+    switch (L.B) {
+      case 12: return run_dequant<2, 12>(L, w, s);
+      case 15: return run_dequant<2, 15>(L, w, s);
+      case 16: return run_dequant<2, 16>(L, w, s);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (L.M) {
     case 1: return run_dequant<1, 8>(L, w, s);
     case 2: return run_dequant<2, 8>(L, w, s);

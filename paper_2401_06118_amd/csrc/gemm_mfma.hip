@@ -15,8 +15,9 @@
 // blocks of 16 tokens and each B fragment for RB blocks of 16 rows.
 //
 // Codeword lookups use the same LDS codebook copies as the matrix-vector
-// kernel (B = 8) or 16-byte L2 gathers (B = 16).  Supported: B = 8 with
-// M in {1, 2, 4, 8} (M divides the 32 codes of a K-tile) and B = 16 with M = 1.
+// kernel (B = 8) or 16-byte L2 gathers (wider codes).  Supported: B = 8 with
+// M in {1, 2, 4, 8} (M divides the 32 codes of a K-tile) and the wide-code
+// formats with M in {1, 2}.
 #include "common.h"
 #include "launch.h"
 
@@ -180,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
           const uint32_t addr = ((uint32_t)(m * 256) + code) * (uint32_t)(C::kCopies * 16) + copy_off;
           v = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb_lds) + addr);
         } else {
-          v = cb[code];
+          v = cb[((uint32_t)m << B) + code];
         }
         const h8_t af = __builtin_bit_cast(h8_t, v);
 #pragma unroll
@@ -259,13 +260,20 @@ hipError_t run_vec(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hi
 }  // namespace
 
 bool mfma_supported(const Layer& L) {
-  if (L.B > 8) return L.M == 1;
+  if (L.B > 8) return L.M == 1 || L.M == 2;
   return L.M == 1 || L.M == 2 || L.M == 4 || L.M == 8;
 }
 
 hipError_t launch_gemm_mfma(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s) {
-  if (L.B == 16) return run_vec<1, 16>(L, n, x, y, s);
-  if (L.B == 15) return run_vec<1, 15>(L, n, x, y, s);
+  if (L.B > 8) {
+    if (L.M == 1) return L.B == 16 ? run_vec<1, 16>(L, n, x, y, s) : run_vec<1, 15>(L, n, x, y, s);
+    switch (L.B) {
+      case 12: return run_vec<2, 12>(L, n, x, y, s);
+      case 15: return run_vec<2, 15>(L, n, x, y, s);
+      case 16: return run_vec<2, 16>(L, n, x, y, s);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (L.M) {
     case 1: return run_vec<1, 8>(L, n, x, y, s);
     case 2: return run_vec<2, 8>(L, n, x, y, s);

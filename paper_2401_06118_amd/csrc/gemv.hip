@@ -14,9 +14,9 @@
 // lane l reads copy l % COPIES.  A ds_read_b128 serves 16 lanes per clock
 // from 64 banks; with 16 copies every lane of a 16-lane group hits its own
 // 16-byte bank quad, so random codeword lookups run conflict-free at the
-// full LDS rate (fewer copies for M > 2, where 16 would not fit).  B = 16:
-// the 1 MiB codebook stays in L2 and each lane gathers its codewords with
-// 16-byte global loads.
+// full LDS rate (fewer copies for M > 2, where 16 would not fit).  Wider
+// codes: the codebooks (2^B codewords each, up to 1 MiB) stay in L2 and each
+// lane gathers its codewords with 16-byte global loads.
 #include "common.h"
 #include "launch.h"
 
@@ -163,7 +163,7 @@ __global__ __launch_bounds__(THREADS) void k_gemv(const uint8_t* __restrict__ co
                 const uint32_t addr = ((uint32_t)(m * 256) + code) * (uint32_t)(C::kCopies * 16) + copy_off;
                 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb_lds) + addr);
               } else {
-                v = cb[code];
+                v = cb[((uint32_t)m << B) + code];
               }
               dot8(v, xr[gi], a0, a1, a2, a3);
             }
@@ -209,8 +209,15 @@ static hipError_t run_gemv_v(const Layer& L, const uint16_t* x, uint16_t* y, hip
 }
 
 hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s) {
-  if (L.B == 16) return run_gemv_v<1, 16>(L, x, y, s);
-  if (L.B == 15) return run_gemv_v<1, 15>(L, x, y, s);
+  if (L.B > 8) {
+    if (L.M == 1) return L.B == 16 ? run_gemv_v<1, 16>(L, x, y, s) : run_gemv_v<1, 15>(L, x, y, s);
+    switch (L.B) {
+      case 12: return run_gemv_v<2, 12>(L, x, y, s);
+      case 15: return run_gemv_v<2, 15>(L, x, y, s);
+      case 16: return run_gemv_v<2, 16>(L, x, y, s);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (L.M) {
     case 1: return run_gemv_v<1, 8>(L, x, y, s);
     case 2: return run_gemv_v<2, 8>(L, x, y, s);

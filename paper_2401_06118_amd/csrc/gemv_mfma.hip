@@ -13,9 +13,11 @@
 // item is 16 rows x one K-slice of 4 x kCPL codes (kCPL = 16 codes, 16 bytes,
 // per lane); lane (r, s) streams the codes [s*kCPL, s*kCPL + kCPL) of the
 // slice for row r with one 16-byte load.  Three kernels:
-//   k_gemv_mfma (B = 16, small launches): items dealt round-robin to the
-//     waves, one accumulator per wave, stored to LDS whenever its row block
-//     changes; codewords gathered from L2;
+//   k_gemv_mfma (codes wider than 8 bits: one codebook in small launches,
+//     two codebooks always): items dealt round-robin to the waves, one
+//     accumulator per wave, stored to LDS whenever its row block changes;
+//     codewords gathered from L2, or from one LDS copy of two 12-bit
+//     codebooks (128 KiB);
 //   k_gemv_ks (B = 8): each wave owns whole K-slices of all the workgroup's
 //     row blocks and keeps one accumulator per block;
 //   k_gemv_cb (B = 16, large launches): the k_gemv_ks split with the codes
@@ -28,9 +30,10 @@
 // stream; all NI code loads of a wave are then in flight at once.  While
 // they arrive the codebooks are copied COPIES times into LDS (lane l reads
 // copy l % COPIES, so 16 lanes hit 16 different 16-byte bank quads) and x is
-// staged in LDS, zero-padded to whole K-slices.  A B = 16 codebook (1 MiB)
-// either stays in L2 and is gathered with 16-byte global loads, or passes
-// through LDS chunk by chunk (k_gemv_cb).
+// staged in LDS, zero-padded to whole K-slices.  Codebooks of wider codes
+// (2^B codewords, up to 1 MiB each) either stay in L2 and are gathered with
+// 16-byte global loads, or, for a single codebook, pass through LDS chunk by
+// chunk (k_gemv_cb).
 //
 // Several independent problems with the same (M, B) can share one launch
 // (e.g. the q, k, v projections of a layer): workgroups are dealt to the
@@ -77,7 +80,12 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
   const int nk = items > wave ? (items - wave + kWaves - 1) / kWaves : 0;
   const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * pitch;
 
-  constexpr int kCbEntries = (B == 8) ? M * 256 * COPIES : 0;
+  // Wide codes with COPIES = 1: the M codebooks sit whole in LDS, one copy
+  // (two 4096-entry codebooks are 128 KiB).
+  constexpr bool kWideLds = B > 8 && COPIES > 0;
+  static_assert(!kWideLds || (COPIES == 1 && (M << B) * 16 <= 128 * 1024), "wide codebooks: one copy, 128 KiB");
+  constexpr int kCbEntries = (B == 8) ? M * 256 * COPIES : (kWideLds ? (M << B) : 0);
+  constexpr int kWideLoads = kWideLds ? kCbEntries / kThreads : 1;  // codebook loads per thread
   uint4* cb_lds = lds;
   uint4* x_lds = lds + kCbEntries;
   float* part = reinterpret_cast<float*>(x_lds + bt.xg_max);
@@ -87,6 +95,11 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
   uint4 cbv = make_uint4(0, 0, 0, 0);
   if constexpr (B == 8) {
     if (tid < M * 256) cbv = cb[tid];
+  }
+  uint4 cbw[kWideLoads];
+  if constexpr (kWideLds) {
+#pragma unroll
+    for (int i = 0; i < kWideLoads; ++i) cbw[i] = cb[tid + i * kThreads];
   }
   // this thread's output row scale, needed only at the end (an unconditional
   // load of a clamped row, so that nothing waits for it here)
@@ -136,6 +149,10 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
       for (int k = 0; k < COPIES; ++k) cb_lds[tid * COPIES + ((k + lane) % COPIES)] = cbv;
     }
   }
+  if constexpr (kWideLds) {
+#pragma unroll
+    for (int i = 0; i < kWideLoads; ++i) cb_lds[tid + i * kThreads] = cbw[i];
+  }
 #pragma unroll
   for (int i = 0; i < C::kXL; ++i) {
     const int grp = tid + i * kThreads;
@@ -164,14 +181,16 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
       const int k = k0 + u;
       const uint32_t cw[4] = {buf[u][0], buf[u][1], buf[u][2], buf[u][3]};
       uint4 av[C::kCPL];
-      if constexpr (B > 8) {
+      if constexpr (B > 8 && !kWideLds) {
         // L2 gathers go out before the next code load so that waiting for
-        // them does not wait for HBM.
+        // them does not wait for HBM.  Code t of a slot belongs to codebook
+        // t % M (2^B codewords of 16 bytes each).
         if (k < nk) {
 #pragma unroll
           for (int t = 0; t < C::kCPL; ++t)
-            av[t] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb) +
-                                                     (((cw[t / 2] >> (16 * (t % 2))) & code_mask(B)) << 4));
+            av[t] = *reinterpret_cast<const uint4*>(
+                reinterpret_cast<const char*>(cb) + ((uint32_t)(t % M) << (B + 4)) +
+                (((cw[t / 2] >> (16 * (t % 2))) & code_mask(B)) << 4));
         }
       }
       issue(f_rb, f_ks, buf[u]);
@@ -197,6 +216,13 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
               const int t = t0 + uu;
               const uint32_t addr = cw_addr<M, COPIES>(cw[t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M);
               av[t] = lds_load16(addr);
+            }
+          } else if constexpr (kWideLds) {
+#pragma unroll
+            for (int uu = 0; uu < 4; ++uu) {
+              const int t = t0 + uu;
+              av[t] = lds_load16(cb_base + ((uint32_t)(t % M) << (B + 4)) +
+                                 (((cw[t / 2] >> (16 * (t % 2))) & code_mask(B)) << 4));
             }
           }
 #pragma unroll
@@ -769,7 +795,8 @@ hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStrea
 }  // namespace
 
 bool gemv_mfma_supported(int M, int B) {
-  return ((B == 15 || B == 16) && M == 1) || (B == 8 && (M == 1 || M == 2 || M == 4));
+  if (B > 8) return format_supported(M, B);
+  return B == 8 && (M == 1 || M == 2 || M == 4);
 }
 
 // Whether x (staged whole in LDS, at most kXL groups per thread) and the
@@ -802,10 +829,11 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     total_bytes += (double)Ls[i].d_out * Ls[i].G * M * code_bytes(B);
   }
   const int cus = num_cus();
-  // 1x16 runs the chunked-codebook kernel where its code items fit in
-  // registers and x next to the chunk (NKS K-slices per wave).
+  // One codebook of wide codes runs the chunked-codebook kernel where its
+  // code items fit in registers and x next to the chunk (NKS K-slices per
+  // wave).  Two codebooks gather from L2.
   int cb_nks = 0;
-  if (B > 8 && vec) {
+  if (B > 8 && M == 1 && vec) {
     for (int i = 0; i < count; ++i) {
       const int KS = (int)(((int64_t)Ls[i].G * 2 + 63) / 64);
       const int nks = (KS + kWaves - 1) / kWaves;
@@ -898,9 +926,25 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     return B == 15 ? launch_cb_shape<15>(bt, cb_nks, rb_max, s) : launch_cb_shape<16>(bt, cb_nks, rb_max, s);
   if (B > 8) {
     if (base > limit) return hipErrorInvalidValue;
-    if (B == 15)
-      return vec ? launch_copies<1, 15, 0, true>(bt, ni, base, s) : launch_copies<1, 15, 0, false>(bt, ni, base, s);
-    return vec ? launch_copies<1, 16, 0, true>(bt, ni, base, s) : launch_copies<1, 16, 0, false>(bt, ni, base, s);
+#define AQLM_GEMV_L2(MM, BB) \
+  return vec ? launch_copies<MM, BB, 0, true>(bt, ni, base, s) : launch_copies<MM, BB, 0, false>(bt, ni, base, s);
+    if (M == 1) {
+      if (B == 15) AQLM_GEMV_L2(1, 15)
+      AQLM_GEMV_L2(1, 16)
+    }
+    // two 4096-entry codebooks (128 KiB) fit in LDS next to x (d_in up to
+    // about 12000) and the partials: gathered from there instead of L2
+    const size_t wide12 = (size_t)(2 << 12) * 16;
+    if (B == 12 && base + wide12 <= limit)
+      return vec ? launch_copies<2, 12, 1, true>(bt, ni, base + wide12, s)
+                 : launch_copies<2, 12, 1, false>(bt, ni, base + wide12, s);
+    switch (B) {
+      case 12: AQLM_GEMV_L2(2, 12)
+      case 15: AQLM_GEMV_L2(2, 15)
+      case 16: AQLM_GEMV_L2(2, 16)
+    }
+#undef AQLM_GEMV_L2
+    return hipErrorInvalidValue;
   }
   // the most codebook copies that fit next to x and the partials
   const size_t per_copy = (size_t)M * 256 * 16;

@@ -8,8 +8,18 @@
 
 namespace aqlm {
 
+// The (M, B) formats the library runs, all with g = 8: one to eight
+// codebooks of 8-bit codes; one codebook of 15- or 16-bit codes; two
+// codebooks of 12-, 15- or 16-bit codes (the 2-, 3- and 4-bit settings of the
+// appendix "Experimental Configurations").  Codes wider than 8 bits are
+// stored one per uint16.
+constexpr bool format_supported(int M, int B) {
+  return (B == 8 && M >= 1 && M <= 8) || ((B == 15 || B == 16) && M == 1) ||
+         ((B == 12 || B == 15 || B == 16) && M == 2);
+}
+
 struct Layer {
-  const void* codes;          // [d_out][G][M] uint8 (B = 8) or uint16 (B = 16)
+  const void* codes;          // [d_out][G][M] uint8 (B = 8) or uint16 (B > 8)
   const uint16_t* codebooks;  // [M][2^B][8] fp16
   const uint16_t* scales;     // [d_out] fp16
   int32_t d_out;

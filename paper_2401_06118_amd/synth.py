@@ -95,13 +95,15 @@ def device_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, n
     """The same distributions drawn on the GPU with torch's seeded generator
     (for multi-GiB benchmark workloads; the bytes differ from :func:`layer`).
     Returns (codes, codebooks, scales, x) as torch tensors on ``device``;
-    codes are uint8 (B <= 8) or int16 holding uint16 bit patterns (B = 16)."""
+    codes are uint8 (B <= 8) or int16 holding uint16 bit patterns (B > 8)."""
     import torch
 
     gen = torch.Generator(device=device)
     gen.manual_seed(seed)
     if B <= 8:
         codes = torch.randint(0, 1 << B, (d_out, d_in // g, M), dtype=torch.uint8, device=device, generator=gen)
+    elif B < 16:
+        codes = torch.randint(0, 1 << B, (d_out, d_in // g, M), dtype=torch.int16, device=device, generator=gen)
     else:
         codes = torch.randint(-(1 << 15), 1 << 15, (d_out, d_in // g, M), dtype=torch.int16, device=device,
                               generator=gen)

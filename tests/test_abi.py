@@ -94,8 +94,10 @@ def test_unsupported_formats(lib, fn):
     assert fn(lib, g=4, d_in=64) == UNSUP
     assert fn(lib, M=0) == UNSUP
     assert fn(lib, M=9) == UNSUP
-    assert fn(lib, M=2, B=16) == UNSUP
-    assert fn(lib, M=2, B=15) == UNSUP
+    assert fn(lib, M=3, B=16) == UNSUP
+    assert fn(lib, M=4, B=12) == UNSUP
+    assert fn(lib, M=2, B=13) == UNSUP
+    assert fn(lib, M=2, B=14) == UNSUP
     assert fn(lib, M=1, B=12) == UNSUP
     assert fn(lib, M=1, B=14) == UNSUP
     assert fn(lib, M=1, B=4) == UNSUP
@@ -130,7 +132,7 @@ def test_grouped_validation(lib):
     assert lib.aqlm_gemv_grouped(None, 1, 2, 8, 8, None) == NULL
     assert lib.aqlm_gemv_grouped(arr, 0, 2, 8, 8, None) == SHAPE
     assert lib.aqlm_gemv_grouped(arr, 9, 2, 8, 8, None) == SHAPE
-    assert lib.aqlm_gemv_grouped(arr, 2, 2, 16, 8, None) == UNSUP
+    assert lib.aqlm_gemv_grouped(arr, 2, 3, 16, 8, None) == UNSUP
     bad = (Prob * 3)(good, Prob(P, P, P, P, P, 64, 60), good)
     assert lib.aqlm_gemv_grouped(bad, 3, 2, 8, 8, None) == SHAPE
     bad = (Prob * 2)(good, Prob(P, P, P, None, P, 64, 64))

@@ -539,3 +539,75 @@ def test_1x15_high_code_bits_are_ignored():
     torch.cuda.synchronize()
     assert torch.equal(y.view(torch.int16), y_hi.view(torch.int16))
     assert torch.equal(w.view(torch.int16), w_hi.view(torch.int16))
+
+
+# ------------------------------- two codebooks of 12-, 15- and 16-bit codes
+# (the 3- and 4-bit settings of the appendix "Experimental Configurations";
+# codes stored one per uint16, m fastest)
+
+@pytest.mark.parametrize("B", [12, 15, 16])
+@pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (11008, 4096), (4096, 11008), (1000, 4104), (37, 8),
+                                        (64, 16384), (24, 65544)])
+def test_2xwide_gemv_matches_oracle(B, d_out, d_in):
+    """The matrix-core kernel with the codebooks in LDS (2x12 up to d_in =
+    11008) or gathered from L2 (2x15, 2x16, and 2x12 at d_in = 16384, where x
+    leaves no room for them), aligned and unaligned code rows; for d_in past
+    its x staging, the vector-ALU kernel."""
+    print(f"[2x{B} gemv] {d_out}x{d_in}", flush=True)
+    lay = synth.layer(17_000 + 100 * B + d_out + d_in, d_out, d_in, 2, B)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemv(codes, cb, sc, x[0])
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y)[None, :])
+
+
+@pytest.mark.parametrize("B", [12, 16])
+def test_2xwide_grouped_matches_oracle(B):
+    _grouped_case([(4096, 4096), (1024, 4096), (1024, 4096)], 2, B, 17_500 + B)
+    _grouped_case([(11008, 4096)] * 2, 2, B, 17_600 + B)
+
+
+@pytest.mark.parametrize("B", [12, 15, 16])
+@pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (1000, 4104)])
+def test_2xwide_dequantize_bit_exact(B, d_out, d_in):
+    lay = synth.layer(17_700 + B + d_out, d_out, d_in, 2, B)
+    assert_bits_equal(dequant_gpu(lay), oracle.dequantize(lay.codes, lay.codebooks, lay.scales))
+
+
+def test_2x12_dequantize_special_values_bit_exact():
+    """Subnormals, ties, signed zeros and overflow through the fp32 sum of two
+    codewords and the scale."""
+    lay = synth.special_layer(17_800, 300, 1024, 2, 12)
+    assert_bits_equal(dequant_gpu(lay), oracle.dequantize(lay.codes, lay.codebooks, lay.scales))
+
+
+@pytest.mark.parametrize("B", [12, 16])
+@pytest.mark.parametrize("n", [4, 16, 32, 100, 300])
+def test_2xwide_gemm_matches_oracle(B, n):
+    """Small batch (chunks of 16), the tiled kernel, and the workspace path."""
+    print(f"[2x{B} gemm] n={n}", flush=True)
+    lay = synth.layer(17_900 + B + n, 1100, 2048, 2, B, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y1 = aq().gemm_small_batch(codes, cb, sc, x)
+    y2 = aq().gemm(codes, cb, sc, x)
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y1))
+    check_products(lay, fp16_to_np(y2))
+
+
+def test_2x12_high_code_bits_are_ignored():
+    """Codes are taken modulo 2^12: setting bits 12-15 of every code changes
+    nothing (no codeword outside a 4096-entry codebook is read)."""
+    lay = synth.layer(18_000, 512, 1024, 2, 12, n=4)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemv(codes, cb, sc, x[0])
+    yb = aq().gemm_small_batch(codes, cb, sc, x)
+    w = aq().dequantize(codes, cb, sc)
+    high = (codes.view(torch.int16) | torch.tensor(-4096, dtype=torch.int16, device="cuda")).contiguous()
+    y_hi = aq().gemv(high, cb, sc, x[0])
+    yb_hi = aq().gemm_small_batch(high, cb, sc, x)
+    w_hi = aq().dequantize(high, cb, sc)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16), y_hi.view(torch.int16))
+    assert torch.equal(yb.view(torch.int16), yb_hi.view(torch.int16))
+    assert torch.equal(w.view(torch.int16), w_hi.view(torch.int16))
