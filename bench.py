@@ -307,15 +307,16 @@ def single_layer_rows(aq, torch):
 
 
 def batch_rows(aq, torch, cases=None):
-    """11008x4096 1x16 and 4x8 with n activation rows (the small-batch and
-    prefill path), plus dequantization of the same layers.  ``cases``, a list
-    of (M, B, n), restricts the run to those products (no dequantization)."""
+    """11008x4096 1x16, 4x8, 2x12 and 2x16 with n activation rows (the small-batch
+    and prefill path), plus dequantization of the same layers.  ``cases``, a
+    list of (M, B, n), restricts the run to those products (no
+    dequantization)."""
     rows = []
-    for M, B in ((1, 16), (4, 8)):
+    for M, B in ((1, 16), (4, 8), (2, 12), (2, 16)):
         for n in (1, 4, 16, 256, 2048):
             from paper_2401_06118_amd import format as fmt
             shp = fmt.AqlmShape(11008, 4096, M, B)
-            name = f"11008x4096 {M}x{B // 8 * 8 if B == 8 else 16}"
+            name = f"11008x4096 {M}x{B}"
             if cases is None or (M, B, n) in cases:
                 reps = 1 if n >= 256 else max(2, (1 << 30) // shp.codes_bytes() + 1)
                 layers = [DeviceLayer(800000 + 7 * i + n, 11008, 4096, M, B, n=n) for i in range(reps)]
