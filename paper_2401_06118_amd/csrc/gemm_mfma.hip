@@ -15,7 +15,8 @@
 // blocks of 16 tokens and each B fragment for RB blocks of 16 rows.
 //
 // Codeword lookups use the same LDS codebook copies as the matrix-vector
-// kernel (B = 8) or 16-byte L2 gathers (wider codes).  Supported: B = 8 with
+// kernel (B = 8), one LDS copy of two 12-bit codebooks (2x12, 128 KiB), or
+// 16-byte L2 gathers (other wide codes).  Supported: B = 8 with
 // M in {1, 2, 4, 8} (M divides the 32 codes of a K-tile) and the wide-code
 // formats with M in {1, 2}.
 #include "common.h"
@@ -34,6 +35,8 @@ struct MfmaCfg {
   static constexpr int kBytesPerCode = code_bytes(B);
   static constexpr int kGT = kQT / M;  // groups (x-slices) per K-tile
   static constexpr int kCopies = (B > 8) ? 0 : (M <= 2 ? 16 : (M <= 4 ? 8 : 4));
+  // two 12-bit codebooks (128 KiB) sit whole in LDS, one copy
+  static constexpr bool kWideLds = (M == 2 && B == 12);
   static constexpr int kLaneBytes = kCPL * kBytesPerCode;  // 8 or 16
   static constexpr int kWords = kLaneBytes / 4;
 };
@@ -88,7 +91,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
   constexpr int kTok = NB * 16;
   constexpr int kPitch = C::kGT + 1;  // uint4 per token row of an x tile (+1 against bank conflicts)
   constexpr int kXTile = kTok * kPitch;
-  constexpr int kLdsCb = (B == 8) ? M * 256 * C::kCopies : 1;
+  constexpr int kLdsCb = (B == 8) ? M * 256 * C::kCopies : (C::kWideLds ? (M << B) : 1);
   constexpr int kXLds = KSPLIT * kXTile;
   constexpr int kRedLds = (KSPLIT > 1) ? (KSPLIT - 1) * kRowGroups * RB * NB * kWave : 0;  // f4_t entries
   __shared__ uint4 cb_lds[kLdsCb];
@@ -123,6 +126,10 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
 #pragma unroll
       for (int k = 0; k < C::kCopies; ++k) cb_lds[e * C::kCopies + ((k + lane) % C::kCopies)] = v;
     }
+  }
+  if constexpr (C::kWideLds) {
+    // (read before the first x tile's barrier, like the 8-bit copies)
+    for (int e = tid; e < kLdsCb; e += kThreads) cb_lds[e] = cb[e];
   }
   const uint32_t copy_off = (B == 8) ? (uint32_t)(lane % (C::kCopies ? C::kCopies : 1)) * 16u : 0u;
 
@@ -180,6 +187,8 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
         if constexpr (B == 8) {
           const uint32_t addr = ((uint32_t)(m * 256) + code) * (uint32_t)(C::kCopies * 16) + copy_off;
           v = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb_lds) + addr);
+        } else if constexpr (C::kWideLds) {
+          v = cb_lds[((uint32_t)m << B) + code];
         } else {
           v = cb[((uint32_t)m << B) + code];
         }
@@ -247,6 +256,10 @@ hipError_t run_shape(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, 
   // Up to 16 tokens: one token block, 16-row workgroups whose four waves split
   // K (many workgroups, like the matrix-vector kernel).  More tokens: 128-row
   // by 64-token tiles, each codeword fragment reused for 4 token blocks.
+  // 2x12 stages 128 KiB of codebooks per workgroup: 64-row workgroups
+  // amortise it (11008x4096, n = 16: 34.8 us, against 59.7 us with 16 rows
+  // and 45.8 us gathering from L2).
+  if (n <= 16 && MfmaCfg<M, B>::kWideLds) return run<M, B, VEC, 4, 1, 4>(L, n, x, y, s);
   if (n <= 16) return run<M, B, VEC, 1, 1, 4>(L, n, x, y, s);
   return run<M, B, VEC, 2, 4, 1>(L, n, x, y, s);
 }
