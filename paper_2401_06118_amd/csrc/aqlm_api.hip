@@ -14,15 +14,22 @@
 
 namespace aqlm {
 
+// Compute units of the current device (cached per device; the work split
+// of every launch is sized by it).
 int num_cus() {
-  static std::atomic<int> cached{0};
-  int v = cached.load(std::memory_order_relaxed);
-  if (v > 0) return v;
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cached[kMaxDevices];
   int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  const bool cacheable = dev >= 0 && dev < kMaxDevices;
+  if (cacheable) {
+    const int v = cached[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+  }
   hipDeviceProp_t prop;
-  if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess) return 256;
-  v = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
-  cached.store(v, std::memory_order_relaxed);
+  if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return 256;
+  const int v = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+  if (cacheable) cached[dev].store(v, std::memory_order_relaxed);
   return v;
 }
 
