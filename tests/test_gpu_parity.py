@@ -38,18 +38,49 @@ def dequant_gpu(lay):
     return w.cpu().numpy().view(np.uint16)
 
 
+def elementwise_bound(w_bits, x, ref):
+    """Largest |y_gpu - y_ref| the GPU arithmetic allows for each output.
+
+    With S = sum_c |W[i,c] x[t,c]| over the oracle's fp16 weights W:
+    - the GPU may skip the fp16 rounding of s_i * (codeword sum), or round
+      fp16 partial products: at most 2^-11 * S each (normal range), plus
+      2^-25 * |x[t,c]| for every W[i,c] in the fp16 subnormal range;
+    - fp32 accumulation over d_in terms in any order (and one more rounding
+      inside v_dot2): at most 2 * d_in * 2^-24 * S;
+    - the fp16 output: half an ulp, at most 2^-11 * |y| plus 2^-25.
+    """
+    w = np.abs(w_bits.view(np.float16).astype(np.float64))
+    xv = np.asarray(x)
+    if xv.dtype == np.uint16:
+        xv = xv.view(np.float16)
+    xa = np.abs(xv.astype(np.float64).reshape(ref.shape[0], -1))
+    d_in = w.shape[1]
+    s = xa @ w.T
+    sub = xa @ (w < 2.0 ** -14).astype(np.float64).T
+    return 2.0 ** -11 * np.abs(ref) + (2.1 * 2.0 ** -11 + 2 * d_in * 2.0 ** -24) * s + 2.0 ** -25 * sub + 2.0 ** -24
+
+
 def check_products(lay, y_gpu, rows=None):
-    """y_gpu: [n, d_out] fp16 numpy.  rows: optional sampled row indices."""
+    """y_gpu: [n, d_out] fp16 numpy.  rows: optional sampled row indices.
+
+    Passes when every token row and the whole output are within relative L2
+    error TOL of the oracle, and every element is within the bound its
+    arithmetic allows (elementwise_bound)."""
     if rows is None:
-        ref = oracle.aqlm_matmul(lay.codes, lay.codebooks, lay.scales, lay.x)
+        w = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
         got = y_gpu
     else:
-        ref = oracle.aqlm_matmul_rows(lay.codes, lay.codebooks, lay.scales, lay.x, rows)
+        w = oracle.dequantize_rows(lay.codes, lay.codebooks, lay.scales, rows)
         got = y_gpu[:, rows]
+    ref = oracle.matmul_f16(w, lay.x)
     assert np.all(np.isfinite(got.astype(np.float64)))
     for t in range(ref.shape[0]):
         assert rel_l2(got[t], ref[t]) <= TOL, (t, rel_l2(got[t], ref[t]))
     assert rel_l2(got, ref) <= TOL
+    err = np.abs(got.astype(np.float64) - ref)
+    bound = elementwise_bound(w, lay.x, ref)
+    worst = np.unravel_index(np.argmax(err - bound), err.shape)
+    assert np.all(err <= bound), ("elementwise", worst, err[worst], bound[worst])
 
 
 # ------------------------------------------------------------------ dequantize
