@@ -34,3 +34,25 @@ def assert_bits_equal(got, ref, what=""):
         show = ", ".join(f"{tuple(int(v) for v in b)}: {int(got[tuple(b)]):#06x} vs {int(ref[tuple(b)]):#06x}"
                          for b in bad[:6])
         raise AssertionError(f"{what}: {len(bad)} of {ref.size} differ; first: {show}")
+
+
+def elementwise_bound(w_bits, x, ref):
+    """Largest |y_gpu - y_ref| the GPU arithmetic allows for each output.
+
+    With S = sum_c |W[i,c] x[t,c]| over the oracle's fp16 weights W:
+    - the GPU may skip the fp16 rounding of s_i * (codeword sum), or round
+      fp16 partial products: at most 2^-11 * S each (normal range), plus
+      2^-25 * |x[t,c]| for every W[i,c] in the fp16 subnormal range;
+    - fp32 accumulation over d_in terms in any order (and one more rounding
+      inside v_dot2): at most 2 * d_in * 2^-24 * S;
+    - the fp16 output: half an ulp, at most 2^-11 * |y| plus 2^-25.
+    """
+    w = np.abs(w_bits.view(np.float16).astype(np.float64))
+    xv = np.asarray(x)
+    if xv.dtype == np.uint16:
+        xv = xv.view(np.float16)
+    xa = np.abs(xv.astype(np.float64).reshape(ref.shape[0], -1))
+    d_in = w.shape[1]
+    s = xa @ w.T
+    sub = xa @ (w < 2.0 ** -14).astype(np.float64).T
+    return 2.0 ** -11 * np.abs(ref) + (2.1 * 2.0 ** -11 + 2 * d_in * 2.0 ** -24) * s + 2.0 ** -25 * sub + 2.0 ** -24

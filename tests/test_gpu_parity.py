@@ -10,7 +10,7 @@ import pytest
 import oracle
 from paper_2401_06118_amd import synth
 
-from helpers import assert_bits_equal, fp16_to_np, rel_l2, to_device
+from helpers import assert_bits_equal, elementwise_bound, fp16_to_np, rel_l2, to_device
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-3
@@ -36,28 +36,6 @@ def dequant_gpu(lay):
     w = aq().dequantize(codes, cb, sc)
     torch.cuda.synchronize()
     return w.cpu().numpy().view(np.uint16)
-
-
-def elementwise_bound(w_bits, x, ref):
-    """Largest |y_gpu - y_ref| the GPU arithmetic allows for each output.
-
-    With S = sum_c |W[i,c] x[t,c]| over the oracle's fp16 weights W:
-    - the GPU may skip the fp16 rounding of s_i * (codeword sum), or round
-      fp16 partial products: at most 2^-11 * S each (normal range), plus
-      2^-25 * |x[t,c]| for every W[i,c] in the fp16 subnormal range;
-    - fp32 accumulation over d_in terms in any order (and one more rounding
-      inside v_dot2): at most 2 * d_in * 2^-24 * S;
-    - the fp16 output: half an ulp, at most 2^-11 * |y| plus 2^-25.
-    """
-    w = np.abs(w_bits.view(np.float16).astype(np.float64))
-    xv = np.asarray(x)
-    if xv.dtype == np.uint16:
-        xv = xv.view(np.float16)
-    xa = np.abs(xv.astype(np.float64).reshape(ref.shape[0], -1))
-    d_in = w.shape[1]
-    s = xa @ w.T
-    sub = xa @ (w < 2.0 ** -14).astype(np.float64).T
-    return 2.0 ** -11 * np.abs(ref) + (2.1 * 2.0 ** -11 + 2 * d_in * 2.0 ** -24) * s + 2.0 ** -25 * sub + 2.0 ** -24
 
 
 def check_products(lay, y_gpu, rows=None):
