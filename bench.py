@@ -1,29 +1,39 @@
 #!/usr/bin/env python3
 """Benchmark of the AQLM token-generation product on one MI355X.
 
-Default workload (one "step"): the linear layers of one Llama-2-7B decode step
-at batch 1 - 32 blocks x {q, k, v, o: 4096x4096; gate, up: 11008x4096; down:
-4096x11008} = 224 AQLM 2x8 (g = 8) matrix-vector products, each layer with
-its own random codes, codebooks, scales and input vector, all resident in HBM,
-launched back to back on one stream.  ``value`` is the step's algorithmic HBM
-bytes (codes + codebooks + scales + x + y of every layer) divided by the
-measured step time; tokens/s-equivalent is 1 / step time (linear layers only:
+Default workload (one "step"): the linear layers of one Llama-2-70B decode
+step at batch 1 on one GPU - 80 blocks x {q, o: 8192x8192; k, v: 1024x8192;
+gate, up: 28672x8192; down: 8192x28672} = 560 AQLM 2x8 (g = 8)
+matrix-vector products (17.16 GB), each layer with its own random codes,
+codebooks, scales and input vector, all resident in HBM, launched back to
+back on one stream as one HIP graph (320 launches: grouped q/k/v, o, grouped
+gate/up, down per block).  ``value`` is the step's algorithmic HBM bytes
+(codes + codebooks + scales + x + y of every layer) divided by the measured
+step time; tokens/s-equivalent is 1 / step time (linear layers only:
 attention, norms, embeddings and the LM head are not part of the step).
 
 Also reported on the same JSON line:
-  roofline      the dominant kernel (the matrix-vector kernel) against 8 TB/s:
-                algorithmic bytes per launch over its average launch duration,
-                the event-timed replay region divided by the launches in it;
-                ``traffic`` is the HBM bytes per launch that the committed
-                rocprofv3 counter summary records for this kernel source
-                (null once the source has changed);
+  roofline      the dominant kernel against 8 TB/s: algorithmic bytes per
+                launch over its average launch duration.  The duration is
+                the one a committed rocprofv3 kernel trace of this command
+                records over the timed graph replays (profiles/
+                kernel_durations.txt, keyed by kernel source digest), or,
+                without one, the event-timed replay region divided by its
+                launches (launch gaps included); both are on the line.
+                ``traffic`` is the HBM bytes per launch from the committed
+                counter summary (null once the source has changed);
   cpu_baseline  the CPU oracle (dequantize + fp64 product) timed on the host
-                cores on a sample of the step's layers, scaled to the step;
-  secondary     the same step in the 1x16 scheme, single layers rotated over
-                >= 1 GiB of replicas (so HBM, not the 256 MB MALL, is measured),
-                the small-batch / prefill products and dequantization.
+                cores on a sample of the step's layers, scaled to the step,
+                with the CPU model and a one-thread time;
+  secondary     the Llama-2-7B steps in 2x8 and 1x16, single layers rotated
+                over >= 1 GiB of replicas (so HBM, not the 256 MB MALL, is
+                measured), the small-batch / prefill products and
+                dequantization.
 
-Only one GPU is supported: --gpus N with N > 1 exits with a message.
+The timed region is bracketed by two short spin kernels outside its events,
+so that ``--summarize-trace`` can pick its dispatches out of a rocprofv3
+kernel trace.  Only one GPU is supported: --gpus N with N > 1 exits with a
+message.
 """
 from __future__ import annotations
 
@@ -58,14 +68,17 @@ def parse_args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="llama2-7b-2x8", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="llama2-70b-2x8", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU-baseline time budget")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="CPU-baseline time budget (all threads)")
     ap.add_argument("--batch-case", metavar="M,B,n[,1]", action="append",
                     help="only time the 11008x4096 product of this format and token count "
                          "(repeatable) and print its row; a fourth field 1 times the workspace "
                          "product (aqlm_gemm) instead")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
+                    help="print per-kernel durations of the dispatches inside the timed region of a "
+                         "rocprofv3 kernel trace (--kernel-trace) of a bench.py run, and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy a few times (the reference kernel for "
                          "scaling HBM byte counters) and exit")
@@ -146,17 +159,29 @@ def graph_of(launches):
     return g
 
 
-def time_steps(fn, steps, warmup):
+MARKER_CYCLES = 20000  # spin kernel that brackets a timed region (about 10 us)
+
+
+def time_steps(fn, steps, warmup, markers=False):
+    """ms per call of fn over `steps` calls bracketed by a HIP event pair on
+    the current stream, after `warmup` untimed calls.  markers: a short spin
+    kernel goes out before the start event and after the end event (outside
+    the timed region) so a kernel trace shows where the region starts and
+    ends."""
     import torch
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
+    if markers:
+        torch.cuda._sleep(MARKER_CYCLES)
     start.record()
     for _ in range(steps):
         fn()
     end.record()
+    if markers:
+        torch.cuda._sleep(MARKER_CYCLES)
     torch.cuda.synchronize()
     return start.elapsed_time(end) / steps  # ms
 
@@ -179,10 +204,12 @@ def step_spread(fn, steps):
 
 
 def per_launch_ms(launches, reps):
-    """Average duration of each launch, from a HIP event pair recorded around it
+    """Average time of each launch between a HIP event pair recorded around it
     on the launching (torch current) stream, over `reps` passes.  Each pass
     starts behind a spin kernel long enough for the host to queue every event
-    and launch first, so the pairs time the GPU, not the host's enqueue rate."""
+    and launch first, so the pairs time the GPU, not the host's enqueue rate.
+    An event pair also counts the dispatch of the launch and the events
+    themselves, so this is an upper bound of the kernel's duration."""
     import torch
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in launches]
           for _ in range(reps)]
@@ -211,23 +238,75 @@ def source_digest(*names):
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel_key: str, digest: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None if there is none for this kernel source."""
-    path = os.path.join(ROOT, "profiles", "traffic.txt")
+def _profile_lookup(fname: str, key: str, digest: str):
+    """Fields after (key, digest) on the matching line of profiles/<fname>."""
+    path = os.path.join(ROOT, "profiles", fname)
     if not os.path.exists(path):
         return None
     for line in open(path):
         parts = line.split()
-        if len(parts) >= 3 and parts[0] == kernel_key and parts[1] == digest:
-            return float(parts[2])
+        if len(parts) >= 3 and parts[0] == key and parts[1] == digest:
+            return parts[2:]
     return None
+
+
+def measured_traffic(kernel_key: str, digest: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None if there is none for this kernel source."""
+    f = _profile_lookup("traffic.txt", kernel_key, digest)
+    return float(f[0]) if f else None
+
+
+def traced_duration(kernel_key: str, digest: str):
+    """(average kernel duration in us, dispatches per step) over the timed
+    graph replays, from the committed rocprofv3 kernel-trace summary of this
+    workload, or None if there is none for this kernel source."""
+    f = _profile_lookup("kernel_durations.txt", kernel_key, digest)
+    return (float(f[0]), float(f[1])) if f else None
+
+
+def summarize_trace(csv_path: str):
+    """Per-kernel durations of the dispatches between the first two marker
+    spin kernels (the timed region of the headline step) of a rocprofv3
+    kernel_trace.csv."""
+    import csv
+    rows = []
+    with open(csv_path, newline="") as f:
+        for r in csv.DictReader(f):
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
+    rows.sort()
+    marks = [i for i, r in enumerate(rows) if "spin_kernel" in r[2]]
+    if len(marks) < 2:
+        raise SystemExit("no pair of marker kernels in the trace")
+    inside = rows[marks[0] + 1:marks[1]]
+    by = {}
+    for t0, t1, name in inside:
+        by.setdefault(name, []).append((t1 - t0) / 1000.0)
+    window_us = (rows[marks[1]][0] - rows[marks[0]][1]) / 1000.0
+    out = {"window_us": window_us, "dispatches": len(inside), "kernels": {}}
+    for name, d in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        d.sort()
+        out["kernels"][name] = {"calls": len(d), "total_us": sum(d), "avg_us": sum(d) / len(d),
+                                "median_us": d[len(d) // 2], "min_us": d[0], "max_us": d[-1]}
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def cpu_baseline(layers, budget_s):
     """Oracle (dequantize + fp64 product) on the host cores, one layer of each
     distinct shape, repeated until the budget is spent; scaled to the step.
-    The two parts are timed separately."""
+    The two parts are timed separately.  Then one pass over the same layers
+    with one thread."""
     import numpy as np
 
     import oracle
@@ -239,10 +318,11 @@ def cpu_baseline(layers, budget_s):
     for key, ls in shapes.items():
         L = ls[0]
         codes = L.codes.cpu().numpy()
-        if L.shape.B == 16:
+        if L.shape.B > 8:
             codes = codes.view(np.uint16)
         host[key] = (codes, L.codebooks.cpu().numpy(), L.scales.cpu().numpy(), L.x.cpu().numpy())
         per_shape[key] = ([], [])
+    threads = oracle.num_threads()
     t_end = time.perf_counter() + budget_s
     rounds = 0
     while True:
@@ -260,16 +340,32 @@ def cpu_baseline(layers, budget_s):
     deq_s = sum(len(shapes[k]) * float(np.median(v[0])) for k, v in per_shape.items())
     mm_s = sum(len(shapes[k]) * float(np.median(v[1])) for k, v in per_shape.items())
     step_s = deq_s + mm_s
+    # one thread, one pass
+    one_s = 0.0
+    try:
+        oracle.set_threads(1)
+        one_threads = oracle.num_threads()
+        for key, (codes, cb, sc, x) in host.items():
+            t0 = time.perf_counter()
+            oracle.matmul_f16(oracle.dequantize(codes, cb, sc), x)
+            one_s += len(shapes[key]) * (time.perf_counter() - t0)
+    finally:
+        oracle.set_threads(threads)
     step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
     return {
         "value": step_bytes / step_s / 1e9,
         "unit": "GB/s",
-        "cores": oracle.num_threads(),
+        "cores": threads,
         "kind": "oracle",
         "sample": (f"one layer of each of the {len(shapes)} distinct shapes, dequantize + fp64 product, "
                    f"median of {rounds} runs each, step time = sum over shapes of count x median "
                    f"({step_s:.3f} s per step, {1.0 / step_s:.4f} tok/s-eq)"),
+        "cpu_model": cpu_model(),
+        "host_cpus": os.cpu_count(),
         "split_s_per_step": {"dequantize": deq_s, "fp64_product": mm_s},
+        "one_thread": {"value": step_bytes / one_s / 1e9, "unit": "GB/s", "threads": one_threads,
+                       "s_per_step": one_s,
+                       "sample": "one run of each distinct shape on one thread, scaled by its count in the step"},
     }
 
 
@@ -294,13 +390,13 @@ def single_layer_rows(aq, torch):
         calls = [lambda L=L: L.gemv(aq) for L in layers]
         g = graph_of(calls)
         ms = time_steps(g.replay, steps=3, warmup=1) / reps
-        kern = per_launch_ms(calls[: min(reps, 64)], reps=2)
-        kern_ms = sum(kern) / len(kern)
+        pair = per_launch_ms(calls[: min(reps, 64)], reps=2)
+        pair_ms = sum(pair) / len(pair)
         del g
         b = shp.gemv_bytes(1)
-        rows.append({"layer": name, "bytes": b, "us_per_call": ms * 1e3, "kernel_us": kern_ms * 1e3,
-                     "GBs_wall": b / (ms * 1e6), "GBs_kernel": b / (kern_ms * 1e6),
-                     "frac_kernel": b / (kern_ms * 1e6) / HBM_PEAK_GBS, "replicas": reps})
+        rows.append({"layer": name, "bytes": b, "us_per_call": ms * 1e3, "frac_per_call": b / (ms * 1e6) / HBM_PEAK_GBS,
+                     "GBs_per_call": b / (ms * 1e6), "event_pair_us": pair_ms * 1e3,
+                     "GBs_event_pair": b / (pair_ms * 1e6), "replicas": reps})
         del layers
         torch.cuda.empty_cache()
     return rows
@@ -379,47 +475,67 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "launches": 5}), flush=True)
 
 
+def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False):
+    """Build a decode step, capture it as one graph and time its replays."""
+    layers = decode_step_layers(model, M, B, seed0)
+    step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
+    launches = launches_by_dependency(layers, aq)
+    graph = graph_of(launches)
+    ms = time_steps(graph.replay, steps, warmup, markers=markers)
+    spread = step_spread(graph.replay, max(steps, 20))
+    return layers, launches, graph, ms, spread, step_bytes
+
+
+def step_seed(M: int) -> int:
+    return 1000 * (1 if M == 2 else 2)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
               "(no multi-GPU path exists).", file=sys.stderr)
         sys.exit(2)
+    if args.summarize_trace:
+        print(json.dumps(summarize_trace(args.summarize_trace)), flush=True)
+        return
     if args.copy_calibration:
         copy_calibration()
         return
     import torch
-    if args.batch_case:
-        import paper_2401_06118_amd as aq
-        from paper_2401_06118_amd import _lib
-        _lib.load()
-        cases = [tuple(int(v) for v in c.split(",")) for c in args.batch_case]
-        print(json.dumps({"batch": batch_rows(aq, torch, cases)}), flush=True)
-        return
-
     import paper_2401_06118_amd as aq
     from paper_2401_06118_amd import _lib
 
     _lib.load()  # fail loudly if the HIP library is missing
+    if args.batch_case:
+        cases = [tuple(int(v) for v in c.split(",")) for c in args.batch_case]
+        print(json.dumps({"batch": batch_rows(aq, torch, cases)}), flush=True)
+        return
+
     model, M, B = WORKLOADS[args.workload]
-    layers = decode_step_layers(model, M, B, seed0=1000 * (1 if M == 2 else 2))
-    step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
-    launches = launches_by_dependency(layers, aq)
-    log(f"{args.workload}: {len(layers)} layers in {len(launches)} launches, {step_bytes / 1e9:.3f} GB per step")
-    graph = graph_of(launches)
-    ms = time_steps(graph.replay, args.steps, args.warmup)
-    spread = step_spread(graph.replay, max(args.steps, 20))
-    log(f"step {ms:.4f} ms (graph replay)")
+    layers, launches, graph, ms, spread, step_bytes = decode_step(
+        model, M, B, step_seed(M), aq, args.steps, args.warmup, markers=True)
+    log(f"{args.workload}: {len(layers)} layers in {len(launches)} launches, {step_bytes / 1e9:.3f} GB per step; "
+        f"step {ms:.4f} ms (graph replay)")
 
     # Dominant kernel: every launch of the step is the matrix-vector kernel
-    # (grouped or single), so its average launch duration is the graph-timed
-    # region (HIP events on the replay stream) divided by the launches in it.
-    avg_launch_ms = ms / len(launches)
+    # (grouped or single).  Its average launch duration comes from the
+    # committed kernel trace of this command when one exists for the current
+    # source; the event-timed replay region divided by its launches (which
+    # includes the gaps between launches) is reported beside it.
     bytes_per_launch = step_bytes / len(launches)
-    achieved = bytes_per_launch / (avg_launch_ms * 1e6)
+    avg_events_us = ms * 1e3 / len(launches)
     digest = source_digest("gemv_mfma.hip", "stream_common.h", "common.h")
     kname = kernel_name(M, B)
-    traffic = measured_traffic(f"{kname}:{args.workload}", digest)
+    key = f"{kname}:{args.workload}"
+    traced = traced_duration(key, digest)
+    if traced is not None:
+        avg_us, source = traced[0], ("rocprofv3 kernel trace of this command over the timed graph replays "
+                                     "(profiles/kernel_durations.txt, same kernel source)")
+    else:
+        avg_us, source = avg_events_us, "HIP events over the timed graph replays / launches (gaps included)"
+    achieved = bytes_per_launch / (avg_us * 1e3)
+    traffic = measured_traffic(key, digest)
 
     result = {
         "metric": "achieved HBM GB/s & roofline % for AQLM GEMV (batch 1); decode tokens/s-equivalent",
@@ -435,7 +551,7 @@ def main():
         "dtype": "f16 (fp32 accumulate)",
         "data": "synthetic: uniform codes, N(0,0.02) fp16 codebooks, U[0.5,1.5] fp16 scales, N(0,1) fp16 x",
         "config": {
-            "workload": f"Llama-2-{model.upper()} decode step, linear layers only, AQLM {M}x{B} "
+            "workload": f"Llama-2-{model.upper()} decode step on one GPU, linear layers only, AQLM {M}x{B} "
                         f"g8, batch 1: {len(layers)} GEMVs in {len(launches)} launches (per block: grouped "
                         f"q/k/v, o, grouped gate/up, down), replayed as one HIP graph",
             "layers": len(layers),
@@ -455,53 +571,55 @@ def main():
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
             "bytes_per_launch": bytes_per_launch,
-            "avg_launch_us": avg_launch_ms * 1e3,
+            "avg_launch_us": avg_us,
+            "duration_source": source,
+            "avg_launch_us_events": avg_events_us,
+            "frac_events": bytes_per_launch / (avg_events_us * 1e3) / HBM_PEAK_GBS,
+            "traced_kernel_ms_per_step": traced[0] * traced[1] / 1e3 if traced else None,
+            "source_digest": digest,
         },
     }
+    del layers, launches, graph
+    torch.cuda.empty_cache()
 
     if not args.no_secondary:
         sec = {}
-        # the same step without grouping: 224 single launches, one graph
-        g1 = graph_of([lambda L=L: L.gemv(aq) for L in layers])
-        ms1 = time_steps(g1.replay, args.steps, 2)
-        sec["ungrouped_224_launches"] = {"ms_per_step": ms1, "GBs": step_bytes / (ms1 * 1e6),
-                                         "tok_s_eq": 1000.0 / ms1}
-        # upper bound without the block's dependencies: 8 independent GEMVs per launch
-        fused = [lambda c=layers[i:i + 8]: aq.gemv_grouped([L.problem() for L in c])
-                 for i in range(0, len(layers), 8)]
-        g8 = graph_of(fused)
-        ms8 = time_steps(g8.replay, args.steps, 2)
-        sec["independent_8_per_launch"] = {"launches": len(fused), "ms_per_step": ms8,
-                                           "GBs": step_bytes / (ms8 * 1e6), "tok_s_eq": 1000.0 / ms8}
-        del g1, g8
-        log(f"ungrouped {ms1:.4f} ms, 8-per-launch {ms8:.4f} ms")
-        other = "llama2-7b-1x16" if args.workload != "llama2-7b-1x16" else "llama2-7b-2x8"
-        om, oM, oB = WORKLOADS[other]
-        del layers, launches, graph
-        torch.cuda.empty_cache()
-        olayers = decode_step_layers(om, oM, oB, seed0=5000)
-        ob = sum(L.shape.gemv_bytes(1) for L in olayers)
-        olaunch = launches_by_dependency(olayers, aq)
-        og = graph_of(olaunch)
-        oms = time_steps(og.replay, max(5, args.steps // 2), 2)
-        okern = per_launch_ms(olaunch, reps=2)
-        sec[other] = {"ms_per_step": oms, "GBs": ob / (oms * 1e6), "frac": ob / (oms * 1e6) / HBM_PEAK_GBS,
-                      "tok_s_eq": 1000.0 / oms, "kernel_sum_ms": sum(okern),
-                      "GBs_kernel": ob / (sum(okern) * 1e6)}
-        del olayers, olaunch, og
-        torch.cuda.empty_cache()
-        log(f"{other}: {oms:.4f} ms per step")
+        for other in ("llama2-7b-2x8", "llama2-7b-1x16"):
+            if other == args.workload:
+                continue
+            om, oM, oB = WORKLOADS[other]
+            ol, olaunch, og, oms, osp, ob = decode_step(om, oM, oB, step_seed(oM) + 4000, aq,
+                                                        max(5, args.steps // 2), 2)
+            pair = per_launch_ms(olaunch, reps=2)
+            row = {"ms_per_step": oms, "GBs": ob / (oms * 1e6), "frac": ob / (oms * 1e6) / HBM_PEAK_GBS,
+                   "tok_s_eq": 1000.0 / oms, "spread": osp, "event_pair_sum_ms": sum(pair),
+                   "GBs_event_pair": ob / (sum(pair) * 1e6)}
+            if oM == 2:
+                # the same step without grouping (224 single launches), and
+                # without the block's dependencies (8 independent GEMVs per launch)
+                g1 = graph_of([lambda L=L: L.gemv(aq) for L in ol])
+                ms1 = time_steps(g1.replay, args.steps, 2)
+                fused = [lambda c=ol[i:i + 8]: aq.gemv_grouped([L.problem() for L in c]) for i in range(0, len(ol), 8)]
+                g8 = graph_of(fused)
+                ms8 = time_steps(g8.replay, args.steps, 2)
+                row["ungrouped_224_launches"] = {"ms_per_step": ms1, "GBs": ob / (ms1 * 1e6)}
+                row["independent_8_per_launch"] = {"launches": len(fused), "ms_per_step": ms8,
+                                                   "GBs": ob / (ms8 * 1e6)}
+                del g1, g8
+            sec[other] = row
+            del ol, olaunch, og
+            torch.cuda.empty_cache()
+            log(f"{other}: {oms:.4f} ms per step")
         sec["single_layers"] = single_layer_rows(aq, torch)
         log("single layers done")
         sec["batch"] = batch_rows(aq, torch)
         log("batch / dequantize done")
         result["secondary"] = sec
-        layers = None
     if not args.no_cpu_baseline:
-        if layers is None:
-            layers = decode_step_layers(model, M, B, seed0=1000 * (1 if M == 2 else 2))
+        layers = decode_step_layers(model, M, B, step_seed(M))
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds)
+        del layers
     print(json.dumps(result), flush=True)
 
 

@@ -55,6 +55,8 @@ def _load():
     lib.oracle_matmul_f16.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_threads.restype = None
     _lib = lib
     return lib
 
@@ -79,7 +81,13 @@ def _check(st: int):
 
 
 def num_threads() -> int:
+    """Threads a parallel region of the oracle runs with."""
     return int(_load().oracle_num_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads for the oracle's later parallel regions (from this thread)."""
+    _load().oracle_set_threads(int(n))
 
 
 def f32_to_f16_bits(values) -> np.ndarray:
@@ -153,7 +161,3 @@ def aqlm_matmul(codes, codebooks, scales, x, g: int = 8) -> np.ndarray:
     """Reference Y[t, i] = sum_c W[i, c] x[t, c] in fp64 with W = dequantize(...); [n, d_out]."""
     return matmul_f16(dequantize(codes, codebooks, scales, g), x)
 
-
-def aqlm_matmul_rows(codes, codebooks, scales, x, rows, g: int = 8) -> np.ndarray:
-    """Reference outputs for the listed rows only: [n, len(rows)]."""
-    return matmul_f16(dequantize_rows(codes, codebooks, scales, rows, g), x)

@@ -210,24 +210,29 @@ int oracle_matmul_f16(const uint16_t* w, int64_t d_out, int64_t d_in, const uint
   return ORC_OK;
 }
 
-/* The whole reference path: dequantize (as above) then the fp64 product.
- * w_scratch must hold d_out * d_in fp16 values; it is left holding W. */
-int oracle_aqlm_matmul(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
-                       int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, const uint16_t* x,
-                       int64_t n, uint16_t* w_scratch, double* y) {
-  int st = oracle_dequantize(codes, codebooks, scales, d_out, d_in, M, B, g, w_scratch);
-  if (st != ORC_OK) return st;
-  return oracle_matmul_f16(w_scratch, d_out, d_in, x, n, y);
-}
-
 #ifdef _OPENMP
 #include <omp.h>
 #endif
-/* Threads the parallel loops above use (1 without OpenMP). */
+/* Threads a parallel region of the loops above actually runs with (1 without
+ * OpenMP). */
 int oracle_num_threads(void) {
+  int n = 1;
 #ifdef _OPENMP
-  return omp_get_max_threads();
+#pragma omp parallel
+  {
+#pragma omp single
+    n = omp_get_num_threads();
+  }
+#endif
+  return n;
+}
+
+/* Threads for later parallel regions started from the calling thread
+ * (n >= 1; ignored without OpenMP). */
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
 #else
-  return 1;
+  (void)n;
 #endif
 }

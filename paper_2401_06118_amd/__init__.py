@@ -60,6 +60,23 @@ def layer_args(codes: torch.Tensor, codebooks: torch.Tensor, scales: torch.Tenso
     return d_out, groups * g, M, B, g
 
 
+def _out(out, shape, like: torch.Tensor) -> torch.Tensor:
+    """A caller's output tensor, checked like the inputs (the C ABI cannot see
+    sizes, so an undersized buffer would be written past its end), or a new
+    one."""
+    if out is None:
+        return torch.empty(shape, dtype=torch.float16, device=like.device)
+    if not isinstance(out, torch.Tensor) or out.dtype != torch.float16 or not out.is_cuda:
+        raise ValueError("out must be an fp16 GPU tensor")
+    if not out.is_contiguous():
+        raise ValueError("out must be contiguous")
+    if tuple(out.shape) != tuple(shape):
+        raise ValueError(f"out must have shape {tuple(shape)}, got {tuple(out.shape)}")
+    if out.device != like.device:
+        raise ValueError("out must be on the same device as the layer")
+    return out
+
+
 def _check(st: int, what: str):
     if st != _lib.AQLM_OK:
         raise AqlmError(st, what)
@@ -68,8 +85,7 @@ def _check(st: int, what: str):
 def dequantize(codes, codebooks, scales, *, out=None, stream=None) -> torch.Tensor:
     """fp16 weight matrix [d_out, d_in]: w[i, 8j+k] = fp16(sum_m C_m[b_ijm][k] * s_i)."""
     d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
-    if out is None:
-        out = torch.empty((d_out, d_in), dtype=torch.float16, device=codes.device)
+    out = _out(out, (d_out, d_in), codes)
     st = _lib.load().aqlm_dequantize(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in,
                                      M, B, g, out.data_ptr(), _stream_handle(stream))
     _check(st, "aqlm_dequantize")
@@ -81,8 +97,7 @@ def gemv(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:
     d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
     if x.dtype != torch.float16 or x.numel() != d_in or not x.is_cuda or not x.is_contiguous():
         raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
-    if out is None:
-        out = torch.empty((d_out,), dtype=torch.float16, device=codes.device)
+    out = _out(out, (d_out,), codes)
     st = _lib.load().aqlm_gemv(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in, M, B, g,
                                x.data_ptr(), out.data_ptr(), _stream_handle(stream))
     _check(st, "aqlm_gemv")
@@ -119,8 +134,7 @@ def gemm_small_batch(codes, codebooks, scales, x, *, out=None, stream=None) -> t
     if x.dtype != torch.float16 or x.dim() != 2 or x.shape[1] != d_in or not x.is_cuda or not x.is_contiguous():
         raise ValueError("x must be a contiguous fp16 GPU tensor [n, d_in]")
     n = x.shape[0]
-    if out is None:
-        out = torch.empty((n, d_out), dtype=torch.float16, device=codes.device)
+    out = _out(out, (n, d_out), codes)
     st = _lib.load().aqlm_gemm_small_batch(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in,
                                            M, B, g, n, x.data_ptr(), out.data_ptr(), _stream_handle(stream))
     _check(st, "aqlm_gemm_small_batch")
@@ -148,8 +162,7 @@ def gemm(codes, codebooks, scales, x, *, workspace=None, out=None, stream=None) 
         raise ValueError("workspace must be a contiguous GPU tensor")
     ws_ptr = workspace.data_ptr() if workspace is not None else None
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    if out is None:
-        out = torch.empty((n, d_out), dtype=torch.float16, device=codes.device)
+    out = _out(out, (n, d_out), codes)
     st = _lib.load().aqlm_gemm(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in, M, B, g, n,
                                x.data_ptr(), out.data_ptr(), ws_ptr, ws_bytes, _stream_handle(stream))
     _check(st, "aqlm_gemm")

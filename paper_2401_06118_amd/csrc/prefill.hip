@@ -1,5 +1,5 @@
 // AQLM product with many activation rows (prefill), on the matrix cores:
-//   Y[t][i] = fp16(s_i * sum_c W~[i][c] X[t][c]),   W~[i, 8j:8j+8] = fp16(sum_m C_m[b_ijm])
+//   Y[t][i] = fp16(s_i * sum_c W~[i][c] X[t][c]),   W~[i, 8j:8j+8] = fp16(fp32 sum_m C_m[b_ijm])
 // (Eq. 2 with the scale taken out of the sum: it multiplies the finished dot
 // product instead of every weight).
 //
@@ -183,14 +183,25 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
             cwv[m] = gcw[s][q];  // gathered one step earlier
           }
         }
-        // Sum of the M codewords in ascending m with packed fp16 adds (four
-        // v_pk_add_f16 per codeword).  Each add rounds to fp16; the product
-        // only has to meet the output tolerance, and the single-rounding fp32
-        // order is kept where the weights themselves are the result
-        // (dequantization).
+        // Sum of the M codewords in fp32, ascending m, rounded once to fp16
+        // (the scale multiplies the finished dot product).  fp16 partial sums
+        // would be cheaper but each would round relative to the partial sum,
+        // not to the weight: codewords that cancel would then lose the weight
+        // entirely.
         h8_t wsum = __builtin_bit_cast(h8_t, cwv[0]);
+        if constexpr (M > 1) {
+          float f[8];
 #pragma unroll
-        for (int m = 1; m < M; ++m) wsum += __builtin_bit_cast(h8_t, cwv[m]);
+          for (int e = 0; e < 8; ++e) f[e] = (float)wsum[e];
+#pragma unroll
+          for (int m = 1; m < M; ++m) {
+            const h8_t cm = __builtin_bit_cast(h8_t, cwv[m]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) f[e] += (float)cm[e];
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) wsum[e] = (_Float16)f[e];
+        }
         uint4 w = __builtin_bit_cast(uint4, wsum);
         if (!row_ok || g + q >= G) w = make_uint4(0, 0, 0, 0);
         at[q] = w;

@@ -90,6 +90,31 @@ def special_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, 
     return Layer(codes, codebooks, scales, x, M, B, g)
 
 
+def cancelling_layer(seed: int, d_out: int, d_in: int, M: int = 4, g: int = 8, n: int = 1,
+                     big: float = 0.5, small: float = 0.004) -> Layer:
+    """8-bit codes whose codewords cancel in pairs: codebook 2k holds random
+    vectors of size ``big``, codebook 2k + 1 their negations plus a ``small``
+    random vector, and the code of codebook 2k + 1 repeats that of 2k.  Every
+    weight group is then a small vector built from large codewords, so an
+    implementation that rounds partial sums (or per-codebook contributions)
+    relative to their own magnitude loses the weight.  M must be even."""
+    if M % 2 or d_in % g:
+        raise ValueError("M must be even and d_in a multiple of g")
+    rng = np.random.default_rng(seed)
+    cb = np.empty((M, 256, g), dtype=np.float16)
+    codes = np.empty((d_out, d_in // g, M), dtype=np.uint8)
+    for k in range(0, M, 2):
+        r = rng.normal(0.0, big, size=(256, g)).astype(np.float16)
+        cb[k] = r
+        cb[k + 1] = (-r.astype(np.float32) + rng.normal(0.0, small, size=(256, g))).astype(np.float16)
+        c = rng.integers(0, 256, size=(d_out, d_in // g), dtype=np.uint8)
+        codes[:, :, k] = c
+        codes[:, :, k + 1] = c
+    scales = rng.uniform(0.5, 1.5, size=d_out).astype(np.float16)
+    x = rng.standard_normal((n, d_in)).astype(np.float16)
+    return Layer(codes, cb, scales, x, M, 8, g)
+
+
 def device_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, n: int = 1,
                  device="cuda", cb_std: float = 0.02):
     """The same distributions drawn on the GPU with torch's seeded generator

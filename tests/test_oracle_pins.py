@@ -305,6 +305,24 @@ def test_matmul_against_exact_sums():
             assert abs(y[t, i] - exact) <= 200 * np.finfo(np.float64).eps * np.abs(terms).sum()
 
 
+def test_thread_count_changes_nothing():
+    """The parallel loops split rows only: one thread and all threads give
+    bit-identical weights and products, and the thread setting takes."""
+    lay = synth.layer(15, 96, 512, 2, 8, n=3)
+    full = oracle.num_threads()
+    try:
+        oracle.set_threads(1)
+        assert oracle.num_threads() == 1
+        w1 = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+        y1 = oracle.matmul_f16(w1, lay.x)
+    finally:
+        oracle.set_threads(full)
+    assert oracle.num_threads() == full
+    wn = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+    assert np.array_equal(w1, wn)
+    assert np.array_equal(y1, oracle.matmul_f16(wn, lay.x))
+
+
 def test_argument_errors():
     lay = synth.layer(1, 4, 16, 1, 8)
     with pytest.raises(TypeError):
