@@ -79,6 +79,11 @@ def parse_args():
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV",
                     help="print per-kernel durations of the dispatches inside the timed region of a "
                          "rocprofv3 kernel trace (--kernel-trace) of a bench.py run, and exit")
+    ap.add_argument("--compare-paths", action="store_true",
+                    help="only time the batch-1 2x8 launches of the Llama-2-70B step (and a 65536x8192 layer) "
+                         "through both kernel families (codeword gathers, partial-product tables) and exit")
+    ap.add_argument("--once", action="store_true",
+                    help="with --compare-paths: launch each family once per case, untimed (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy a few times (the reference kernel for "
                          "scaling HBM byte counters) and exit")
@@ -459,6 +464,56 @@ def kernel_name(M: int, B: int) -> str:
     return "aqlm::k_gemv"
 
 
+PATH_CASES = {
+    # name: shapes of one grouped launch (2x8)
+    "70b gate/up": [(28672, 8192)] * 2,
+    "70b down": [(8192, 28672)],
+    "70b q/k/v": [(8192, 8192), (1024, 8192), (1024, 8192)],
+    "70b o": [(8192, 8192)],
+    "7b gate/up": [(11008, 4096)] * 2,
+    "65536x8192": [(65536, 8192)],
+}
+
+
+def compare_paths(aq, torch, once=False):
+    """Both kernel families on the same launches: each case's grouped launch
+    rotated over >= 1 GiB of independent layers (so HBM is read), timed per
+    launch from a graph of the rotation; plus the relative L2 difference of
+    the two results."""
+    from paper_2401_06118_amd import format as fmt
+    rows = []
+    for name, shapes in PATH_CASES.items():
+        b = sum(fmt.AqlmShape(o, k, 2, 8).gemv_bytes(1) for o, k in shapes)
+        reps = 1 if once else max(2, (1 << 30) // b + 1)
+        sets = []
+        for r in range(reps):
+            ls = [DeviceLayer(600000 + 31 * r + i, o, k, 2, 8) for i, (o, k) in enumerate(shapes)]
+            for L in ls[1:]:
+                if L.x.shape == ls[0].x.shape:
+                    L.x = ls[0].x
+            sets.append(ls)
+        res = {"launch": name, "shapes": shapes, "bytes": b, "replicas": reps}
+        outs = {}
+        for path in ("gather", "table"):
+            calls = [lambda ls=ls, path=path: aq.gemv_grouped([L.problem() for L in ls], path=path) for ls in sets]
+            if once:
+                calls[0]()
+                torch.cuda.synchronize()
+            else:
+                g = graph_of(calls)
+                us = time_steps(g.replay, steps=5, warmup=1) / reps * 1e3
+                del g
+                res[f"{path}_us"] = us
+                res[f"{path}_GBs"] = b / (us * 1e3)
+            outs[path] = [L.y.double().clone() for L in sets[0]]
+        res["rel_l2_diff"] = max(float((a - c).norm() / c.norm()) for a, c in zip(outs["table"], outs["gather"]))
+        rows.append(res)
+        log(f"{name}: " + ", ".join(f"{k} {v:.2f}" for k, v in res.items() if k.endswith("_us")))
+        del sets
+        torch.cuda.empty_cache()
+    return rows
+
+
 COPY_BYTES = 256 << 20
 
 
@@ -507,6 +562,9 @@ def main():
     from paper_2401_06118_amd import _lib
 
     _lib.load()  # fail loudly if the HIP library is missing
+    if args.compare_paths:
+        print(json.dumps({"paths": compare_paths(aq, torch, once=args.once)}), flush=True)
+        return
     if args.batch_case:
         cases = [tuple(int(v) for v in c.split(",")) for c in args.batch_case]
         print(json.dumps({"batch": batch_rows(aq, torch, cases)}), flush=True)

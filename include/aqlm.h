@@ -115,6 +115,29 @@ typedef struct aqlm_gemv_problem {
 int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
                       void* stream);
 
+/* Kernel families for the batch-1 product (aqlm_gemv_grouped_path). */
+enum aqlm_gemv_path {
+  AQLM_PATH_AUTO = 0,   /* the library's choice (what aqlm_gemv / aqlm_gemv_grouped run): the
+                           gather family, measured at least as fast on every Llama-2 shape */
+  AQLM_PATH_GATHER = 1, /* codeword gathers: each code's codeword is looked up and multiplied
+                           with x (matrix-core or vector-ALU kernel, by format and size) */
+  AQLM_PATH_TABLE = 2   /* per-group partial-product tables: the inner products
+                           <C_m[e], x_j> of every codeword e and input group j are
+                           computed once per workgroup (in fp32, on the matrix cores)
+                           and each code adds its table entry (the lookup of precomputed
+                           inner products of Sec. 2.2 applied to Eq. 2).  2x8 only, with
+                           d_in a multiple of 256 */
+};
+
+/* aqlm_gemv_grouped with the kernel family chosen by the caller (for
+ * measurement, or where the caller knows its shapes better).  Same
+ * arguments, results and rules as aqlm_gemv_grouped, plus `path`; a path
+ * that cannot take the format or shapes returns AQLM_ERR_UNSUPPORTED before
+ * anything is launched.  Both families accumulate in fp32 and meet the same
+ * accuracy; their results differ in the last bits.  Deterministic. */
+int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                           int32_t path, void* stream);
+
 /* Product with n activation rows: y[t][i] = fp16(s_i * sum_c W[i][c] x[t][c])
  * with W reconstructed as above, fp32 accumulation, any n >= 1 (the batched
  * and prefill products of a layer; the paper times the single-row case,

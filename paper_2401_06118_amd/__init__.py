@@ -104,9 +104,14 @@ def gemv(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:
     return out
 
 
-def gemv_grouped(problems, *, stream=None):
+def gemv_grouped(problems, *, path: str = "auto", stream=None):
     """Independent products [(codes, codebooks, scales, x, y), ...] sharing (M, B)
-    in one launch; each y [d_out] is written in place.  Returns the y list."""
+    in one launch; each y [d_out] is written in place.  Returns the y list.
+    ``path``: "auto" (the library's choice), "gather" (codeword gathers) or
+    "table" (per-group partial-product tables; 2x8, d_in % 256 == 0)."""
+    paths = {"auto": _lib.PATH_AUTO, "gather": _lib.PATH_GATHER, "table": _lib.PATH_TABLE}
+    if path not in paths:
+        raise ValueError(f"path must be one of {sorted(paths)}")
     if not 1 <= len(problems) <= _lib.MAX_GROUPED:
         raise ValueError(f"1..{_lib.MAX_GROUPED} problems per grouped launch")
     arr = (_lib.GemvProblem * len(problems))()
@@ -123,8 +128,9 @@ def gemv_grouped(problems, *, stream=None):
             raise ValueError("y must be a contiguous fp16 GPU tensor with d_out elements")
         arr[i] = _lib.GemvProblem(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), x.data_ptr(),
                                   y.data_ptr(), d_out, d_in)
-    st = _lib.load().aqlm_gemv_grouped(arr, len(problems), fmt[0], fmt[1], fmt[2], _stream_handle(stream))
-    _check(st, "aqlm_gemv_grouped")
+    st = _lib.load().aqlm_gemv_grouped_path(arr, len(problems), fmt[0], fmt[1], fmt[2], paths[path],
+                                            _stream_handle(stream))
+    _check(st, "aqlm_gemv_grouped_path")
     return [p[4] for p in problems]
 
 

@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(HERE, "libaqlm_mi355x.so")
 AQLM_OK = 0
 STATUS_NAMES = {0: "AQLM_OK", 1: "AQLM_ERR_NULL", 2: "AQLM_ERR_SHAPE", 3: "AQLM_ERR_UNSUPPORTED",
                 4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP", 6: "AQLM_ERR_WORKSPACE"}
-EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemm_small_batch",
+PATH_AUTO, PATH_GATHER, PATH_TABLE = 0, 1, 2
+EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemv_grouped_path", "aqlm_gemm_small_batch",
            "aqlm_gemm_workspace_bytes", "aqlm_gemm", "aqlm_status_string")
 MAX_GROUPED = 8
 
@@ -58,6 +59,8 @@ def load():
         lib.aqlm_gemv.restype = ctypes.c_int
         lib.aqlm_gemv_grouped.argtypes = [ctypes.POINTER(GemvProblem), i32, i32, i32, i32, p]
         lib.aqlm_gemv_grouped.restype = ctypes.c_int
+        lib.aqlm_gemv_grouped_path.argtypes = [ctypes.POINTER(GemvProblem), i32, i32, i32, i32, i32, p]
+        lib.aqlm_gemv_grouped_path.restype = ctypes.c_int
         lib.aqlm_gemm_small_batch.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p]
         lib.aqlm_gemm_small_batch.restype = ctypes.c_int
         lib.aqlm_gemm_workspace_bytes.argtypes = [i64, i64, i32, i32, i32, i64]

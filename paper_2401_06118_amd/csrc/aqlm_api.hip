@@ -111,9 +111,13 @@ int check_tokens(const uint16_t* x, uint16_t* y, int64_t n, int64_t d_in) {
   return AQLM_OK;
 }
 
-// n = 1: the matrix-core kernel for M in {1, 2, 4} (B = 8) and 1x16 when x
-// fits in its LDS staging (d_in up to 32768 for 8-bit codes, 65536 for
-// 16-bit); the vector-ALU kernel otherwise.
+// n = 1: the matrix-core (codeword gather) kernel for M in {1, 2, 4}
+// (B = 8) and 1x16 when x fits in its LDS staging (d_in up to 32768 for 8-bit
+// codes, 65536 for 16-bit); the vector-ALU kernel otherwise.  The
+// partial-product-table kernel is never chosen here: measured on every
+// Llama-2-7B and 70B launch and on a 65536 x 8192 layer it was no faster (4-7 %
+// slower where a table is shared by 224-256 rows, 1.4-3x slower with fewer),
+// so it runs only when a caller asks for it (aqlm_gemv_grouped_path).
 hipError_t gemv_dispatch(const aqlm::Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s) {
   if (aqlm::gemv_mfma_supported(L.M, L.B) && aqlm::gemv_mfma_fits(&L, 1))
     return aqlm::launch_gemv_mfma(&L, &x, &y, 1, s);
@@ -223,7 +227,13 @@ int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scal
 
 int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
                       void* stream) {
+  return aqlm_gemv_grouped_path(problems, count, M, B, g, AQLM_PATH_AUTO, stream);
+}
+
+int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                           int32_t path, void* stream) {
   if (!problems) return AQLM_ERR_NULL;
+  if (path != AQLM_PATH_AUTO && path != AQLM_PATH_GATHER && path != AQLM_PATH_TABLE) return AQLM_ERR_UNSUPPORTED;
   if (count < 1 || count > AQLM_MAX_GROUPED) return AQLM_ERR_SHAPE;
   aqlm::Layer Ls[AQLM_MAX_GROUPED];
   const uint16_t* xs[AQLM_MAX_GROUPED];
@@ -238,6 +248,10 @@ int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t 
     ys[i] = P.y;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (path == AQLM_PATH_TABLE) {
+    if (!aqlm::gemv_lut_supported(Ls, count)) return AQLM_ERR_UNSUPPORTED;
+    return status_of(aqlm::launch_gemv_lut(Ls, xs, ys, count, s));
+  }
   bool same_class = true;
   for (int i = 1; i < count; ++i) same_class = same_class && Ls[i].vec_codes == Ls[0].vec_codes;
   if (aqlm::gemv_mfma_supported(M, B) && same_class && aqlm::gemv_mfma_fits(Ls, count))

@@ -59,6 +59,11 @@ bool gemv_mfma_fits(const Layer* Ls, int count);
 hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
                             hipStream_t s);
 hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s);
+// Batch-1 2x8 product through per-group partial-product tables (d_in a
+// multiple of 256).
+bool gemv_lut_supported(const Layer* Ls, int count);
+hipError_t launch_gemv_lut(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
+                           hipStream_t s);
 hipError_t launch_gemm_mfma(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
 bool mfma_supported(const Layer& L);
 bool gemm_nb_supported(const Layer& L, int32_t n);

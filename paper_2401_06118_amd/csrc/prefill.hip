@@ -64,6 +64,35 @@ __device__ __forceinline__ uint32_t code_at(const uint32_t* w, int q) {
   return (w[q / 4] >> (8 * (q % 4))) & 0xFFu;
 }
 
+// fp32 sums of fp16 halves with v_fma_mix (fma(a, 1, c) = a + c, rounded once):
+// mix_add2<H>: half H of a plus half H of b; mix_add<H>: half H of c plus an
+// fp32 value; mix_round2: fp16(c.lo + lo) | fp16(c.hi + hi) << 16, each
+// rounded once from the exact sum.
+template <int H>
+__device__ __forceinline__ float mix_add2(uint32_t a, uint32_t b) {
+  float d;
+  if constexpr (H == 0)
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[0,0,0] op_sel_hi:[1,0,1]" : "=v"(d) : "v"(a), "v"(b));
+  else
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,1] op_sel_hi:[1,0,1]" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+template <int H>
+__device__ __forceinline__ float mix_add(uint32_t c, float acc) {
+  float d;
+  if constexpr (H == 0)
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "=v"(d) : "v"(c), "v"(acc));
+  else
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(d) : "v"(c), "v"(acc));
+  return d;
+}
+__device__ __forceinline__ uint32_t mix_round2(uint32_t c, float lo, float hi) {
+  uint32_t d;
+  asm("v_fma_mixlo_f16 %0, %1, 1.0, %2 op_sel:[0,0,0] op_sel_hi:[1,0,0]" : "=v"(d) : "v"(c), "v"(lo));
+  asm("v_fma_mixhi_f16 %0, %1, 1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "+v"(d) : "v"(c), "v"(hi));
+  return d;
+}
+
 template <int M, int B, int BN, bool VEC>
 __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int32_t tok_tiles) {
   using P = PfCfg<M, B, BN>;
@@ -189,7 +218,23 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
         // not to the weight: codewords that cancel would then lose the weight
         // entirely.
         h8_t wsum = __builtin_bit_cast(h8_t, cwv[0]);
-        if constexpr (M > 1) {
+        if constexpr (M == 4) {
+          // v_fma_mix takes the fp16 halves directly: 6 instructions per
+          // pair of weights (the compiler's convert-add-pack form takes 15)
+          const uint32_t* c0 = reinterpret_cast<const uint32_t*>(&cwv[0]);
+          const uint32_t* c1 = reinterpret_cast<const uint32_t*>(&cwv[1]);
+          const uint32_t* c2 = reinterpret_cast<const uint32_t*>(&cwv[2]);
+          const uint32_t* c3 = reinterpret_cast<const uint32_t*>(&cwv[3]);
+          uint32_t o[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float lo = mix_add2<0>(c0[i], c1[i]), hi = mix_add2<1>(c0[i], c1[i]);
+            lo = mix_add<0>(c2[i], lo);
+            hi = mix_add<1>(c2[i], hi);
+            o[i] = mix_round2(c3[i], lo, hi);
+          }
+          wsum = __builtin_bit_cast(h8_t, make_uint4(o[0], o[1], o[2], o[3]));
+        } else if constexpr (M > 1) {
           float f[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) f[e] = (float)wsum[e];

@@ -159,3 +159,20 @@ def test_gemm_workspace(lib):
     assert gemm_ws(lib, ws_bytes=need - 1) == WORKSPACE
     assert gemm_ws(lib, ws=P + 8) == ALIGN
     assert gemm_ws(lib, n=0) == SHAPE
+
+
+def test_grouped_path_validation(lib):
+    """aqlm_gemv_grouped_path: unknown paths, and the table path on formats or
+    shapes it does not take, are refused before anything is launched."""
+    Prob = _lib.GemvProblem
+    good = Prob(P, P, P, P, P, 64, 64)
+    arr = (Prob * 2)(good, good)
+    for path in (-1, 3, 100):
+        assert lib.aqlm_gemv_grouped_path(arr, 2, 2, 8, 8, path, None) == UNSUP
+    assert lib.aqlm_gemv_grouped_path(arr, 2, 2, 8, 8, 2, None) == UNSUP      # d_in not a multiple of 256
+    wide = (Prob * 1)(Prob(P, P, P, P, P, 64, 512))
+    assert lib.aqlm_gemv_grouped_path(wide, 1, 1, 16, 8, 2, None) == UNSUP    # 1x16
+    assert lib.aqlm_gemv_grouped_path(wide, 1, 4, 8, 8, 2, None) == UNSUP     # 4x8
+    assert lib.aqlm_gemv_grouped_path(None, 1, 2, 8, 8, 0, None) == NULL
+    bad = (Prob * 1)(Prob(P, P, P, P, P, 64, 60))
+    assert lib.aqlm_gemv_grouped_path(bad, 1, 2, 8, 8, 2, None) == SHAPE

@@ -473,6 +473,116 @@ def test_gemv_grouped_70b_qkv():
         check_products(lay, fp16_to_np(y)[None, :])
 
 
+# The partial-product-table kernel (2x8, d_in a multiple of 256), asked for
+# explicitly: tall layers, ragged row counts, grouped.
+LUT_CASES = [
+    [(60000, 256)],                      # ragged last workgroup (235 rows each)
+    [(49155, 512)],                      # row count not a multiple of 4
+    [(65536, 1024)],                     # 256 rows per workgroup (four quads per wave)
+    [(30000, 768), (30001, 768)],        # grouped, ragged
+    [(50000, 2816)],                     # 11 K-slices: odd count, ring tail
+]
+
+
+@pytest.mark.parametrize("shapes", LUT_CASES)
+def test_gemv_partial_product_tables(shapes):
+    print(f"[lut] {shapes}", flush=True)
+    lays = [synth.layer(8400 + 17 * i + d_out, d_out, d_in, 2, 8) for i, (d_out, d_in) in enumerate(shapes)]
+    if len(lays) > 1:
+        for lay in lays[1:]:
+            lay.x = lays[0].x
+    probs = []
+    for lay in lays:
+        codes, cb, sc, _ = to_device(lay)
+        y = torch.full((lay.d_out,), float("nan"), dtype=torch.float16, device="cuda")
+        probs.append((codes, cb, sc, to_device(lays[0])[3][0], y))
+    aq().gemv_grouped(probs, path="table")
+    torch.cuda.synchronize()
+    for lay, pr in zip(lays, probs):
+        check_products(lay, fp16_to_np(pr[4])[None, :])
+
+
+@pytest.mark.parametrize("shapes", [[(1, 256)], [(5, 512)], [(4096, 4096)] * 3, [(8192, 28672)],
+                                    [(1000, 2048), (64, 256), (3000, 1024)]])
+@pytest.mark.parametrize("path", ["table", "gather"])
+def test_gemv_forced_path(shapes, path):
+    """Either kernel family on shapes the library would give to the other:
+    the table kernel with few rows per workgroup (down to one row), the
+    gather kernel on tall layers."""
+    if path == "gather":
+        shapes = [(60000, 256)] if shapes == [(1, 256)] else shapes
+    print(f"[path] {path} {shapes}", flush=True)
+    lays = [synth.layer(8800 + 13 * i + d_out, d_out, d_in, 2, 8) for i, (d_out, d_in) in enumerate(shapes)]
+    probs = []
+    for lay in lays:
+        codes, cb, sc, x = to_device(lay)
+        probs.append((codes, cb, sc, x[0], torch.full((lay.d_out,), float("nan"), dtype=torch.float16,
+                                                      device="cuda")))
+    aq().gemv_grouped(probs, path=path)
+    torch.cuda.synchronize()
+    for lay, pr in zip(lays, probs):
+        check_products(lay, fp16_to_np(pr[4])[None, :])
+
+
+def test_gemv_table_path_refused_where_unsupported():
+    lay = synth.layer(8900, 64, 520, 2, 8)
+    codes, cb, sc, x = to_device(lay)
+    y = torch.full((64,), 5.0, dtype=torch.float16, device="cuda")
+    with pytest.raises(aq().AqlmError):
+        aq().gemv_grouped([(codes, cb, sc, x[0], y)], path="table")
+    torch.cuda.synchronize()
+    assert torch.all(y == 5.0)
+
+
+@pytest.mark.parametrize("path", ["table", "auto"])
+def test_gemv_partial_product_tables_70b_gate_up(path):
+    """Llama-2-70B gate and up (28672 x 8192 each) as one grouped launch
+    through both kernel families; sampled rows."""
+    lays = [synth.layer(8500 + i, 28672, 8192, 2, 8) for i in range(2)]
+    lays[1].x = lays[0].x
+    x = to_device(lays[0])[3][0]
+    probs = []
+    for lay in lays:
+        codes, cb, sc, _ = to_device(lay)
+        probs.append((codes, cb, sc, x, torch.empty(28672, dtype=torch.float16, device="cuda")))
+    aq().gemv_grouped(probs, path=path)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 1, 2, 3, 28671], np.random.default_rng(4).integers(0, 28672, 96)]))
+    for lay, pr in zip(lays, probs):
+        check_products(lay, fp16_to_np(pr[4])[None, :], rows)
+
+
+def test_gemv_partial_product_tables_cancelling_and_special():
+    """Cancelling codebooks and special-value codebooks through the table
+    kernel."""
+    for lay in (synth.cancelling_layer(8600, 60000, 512, 2), synth.special_layer(8601, 60000, 256, 2, 8)):
+        if not np.all(np.isfinite(lay.codebooks.astype(np.float64))):
+            continue
+        codes, cb, sc, x = to_device(lay)
+        yt = torch.empty(lay.d_out, dtype=torch.float16, device="cuda")
+        aq().gemv_grouped([(codes, cb, sc, x[0], yt)], path="table")
+        y = fp16_to_np(yt)[None, :]
+        w = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+        ref = oracle.matmul_f16(w, lay.x)
+        fin = np.isfinite(ref[0]) & (np.abs(ref[0]) < 6.0e4)
+        if lay.codebooks.max() > 1:  # special values: every finite output within its bound
+            err = np.abs(y.astype(np.float64) - ref)[0][fin]
+            bound = elementwise_bound(w, lay.x, ref, abs_codeword_sums(lay))[0][fin]
+            assert np.all(err <= bound)
+        else:
+            check_products(lay, y)
+
+
+def test_gemv_partial_product_tables_deterministic():
+    lay = synth.layer(8700, 60000, 512, 2, 8)
+    codes, cb, sc, x = to_device(lay)
+    ys = torch.empty((100, 60000), dtype=torch.float16, device="cuda")
+    for i in range(100):
+        aq().gemv_grouped([(codes, cb, sc, x[0], ys[i])], path="table")
+    ys = ys.cpu().numpy().view(np.uint16)
+    assert (ys == ys[0]).all()
+
+
 def test_gemv_grouped_deterministic():
     probs = _grouped_case([(4096, 4096)] * 3, 2, 8, 8100)
     first = [p[4].cpu().numpy().view(np.uint16).copy() for p in probs]
