@@ -67,7 +67,8 @@ enum aqlm_status {
   AQLM_ERR_UNSUPPORTED = 3, /* (M, B, g) outside the supported set */
   AQLM_ERR_ALIGN = 4,       /* a pointer breaks the alignment rule above */
   AQLM_ERR_HIP = 5,         /* the HIP runtime reported an error */
-  AQLM_ERR_WORKSPACE = 6    /* aqlm_gemm: workspace smaller than aqlm_gemm_workspace_bytes */
+  AQLM_ERR_WORKSPACE = 6,   /* aqlm_gemm: workspace smaller than aqlm_gemm_workspace_bytes */
+  AQLM_ERR_SCRATCH = 7      /* aqlm_gemm_noalloc: the product needs more than its fixed scratch */
 };
 
 /* Dequantize: w_out[i][j*g + k] = fp16(fp32(sum_m C_m[b[i][j][m]][k]) * s_i)
@@ -179,6 +180,31 @@ size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t
 int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
               int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n,
               const uint16_t* x, uint16_t* y, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of the fixed device scratch buffer of aqlm_gemm_noalloc (128 MiB). */
+#define AQLM_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/* aqlm_gemm for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same product, computed by the same kernels as aqlm_gemm, with the workspace
+ * taken from a fixed scratch buffer of AQLM_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each device it runs on (a static device array, allocated
+ * when the library's code is loaded on the device and kept until the process
+ * ends).  The call itself allocates nothing.  The caller passes inputs and
+ * outputs only.  Results are bit-identical to aqlm_gemm's.
+ *   - The scratch needed is aqlm_gemm_workspace_bytes(...); a product that
+ *     needs more than AQLM_NOALLOC_SCRATCH_BYTES (e.g. more than 64 M weights)
+ *     returns AQLM_ERR_SCRATCH before anything is launched.  When no
+ *     workspace is needed the call computes exactly aqlm_gemm_small_batch.
+ *   - Every call on one device shares that device's buffer, which keeps the
+ *     last call's contents (nothing in it needs to start at zero: each call
+ *     writes what it reads).  Calls that overlap on one device - on two
+ *     streams, or from two host threads without ordering - RACE and give
+ *     undefined results; calls on one stream are ordered and safe.
+ * Other errors as aqlm_gemm; deterministic. */
+int aqlm_gemm_noalloc(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                      int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
+                      void* stream);
 
 /* Static text for a status code (never NULL). */
 const char* aqlm_status_string(int status);

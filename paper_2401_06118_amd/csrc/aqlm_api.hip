@@ -54,6 +54,31 @@ hipError_t allow_dynamic_lds(const void* kern, int bytes) {
 
 namespace {
 
+// Scratch of aqlm_gemm_noalloc: one fixed buffer per device, allocated with
+// the library's code object and held until the process ends.  Host code never
+// uses the array's name as an address (on the host it is only a stand-in):
+// the device address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = AQLM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of this device's scratch array (nullptr on a HIP error),
+// looked up on the first call on each device, with that device current.
+void* scratch_ptr() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  static std::mutex mu;
+  static void* ptrs[kMaxDevices] = {};
+  const std::lock_guard<std::mutex> lock(mu);
+  if (ptrs[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return nullptr;
+    ptrs[dev] = p;
+  }
+  return ptrs[dev];
+}
+
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
 int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
@@ -225,6 +250,27 @@ int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scal
   return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, L.d_out, L.d_in, s));
 }
 
+int aqlm_gemm_noalloc(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                      int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
+                      void* stream) {
+  aqlm::Layer L;
+  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  st = check_tokens(x, y, n, d_in);
+  if (st != AQLM_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (!two_pass(d_in, n)) return gemm_dispatch(L, n, x, y, s);
+  const size_t wbytes = ws_weight_bytes(d_out, d_in);
+  if (wbytes + aqlm::gemm_f16_part_bytes(n, d_out, d_in) > kScratchBytes) return AQLM_ERR_SCRATCH;
+  char* base = static_cast<char*>(scratch_ptr());
+  if (base == nullptr) return AQLM_ERR_HIP;
+  uint16_t* w = reinterpret_cast<uint16_t*>(base);
+  float* part = reinterpret_cast<float*>(base + wbytes);
+  const hipError_t e = aqlm::launch_dequant(L, w, s);
+  if (e != hipSuccess) return AQLM_ERR_HIP;
+  return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, L.d_out, L.d_in, s));
+}
+
 int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
                       void* stream) {
   return aqlm_gemv_grouped_path(problems, count, M, B, g, AQLM_PATH_AUTO, stream);
@@ -272,6 +318,7 @@ const char* aqlm_status_string(int status) {
     case AQLM_ERR_ALIGN: return "misaligned pointer";
     case AQLM_ERR_HIP: return "HIP runtime error";
     case AQLM_ERR_WORKSPACE: return "workspace too small";
+    case AQLM_ERR_SCRATCH: return "needs more scratch than aqlm_gemm_noalloc's fixed buffer holds";
   }
   return "unknown status";
 }

@@ -176,3 +176,19 @@ def test_grouped_path_validation(lib):
     assert lib.aqlm_gemv_grouped_path(None, 1, 2, 8, 8, 0, None) == NULL
     bad = (Prob * 1)(Prob(P, P, P, P, P, 64, 60))
     assert lib.aqlm_gemv_grouped_path(bad, 1, 2, 8, 8, 2, None) == SHAPE
+
+
+def test_noalloc_refuses_before_launch(lib):
+    """aqlm_gemm_noalloc: bad arguments, and a product needing more than the
+    fixed scratch buffer (AQLM_ERR_SCRATCH), are refused on the host."""
+    def call(codes=P, d_out=64, d_in=64, n=64, M=2, B=8, x=P, y=P):
+        return lib.aqlm_gemm_noalloc(codes, P, P, d_out, d_in, M, B, 8, n, x, y, None)
+    assert call(codes=None) == NULL
+    assert call(x=None) == NULL
+    assert call(d_in=60) == SHAPE
+    assert call(n=0) == SHAPE
+    assert call(M=3, B=16) == UNSUP
+    assert call(x=P + 2) == ALIGN
+    assert call(d_out=12288, d_in=8192) == 7            # 192 MiB of weights
+    assert call(d_out=28672, d_in=8192, n=2048) == 7
+    assert lib.aqlm_status_string(7) != b"unknown status"
