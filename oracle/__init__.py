@@ -53,6 +53,8 @@ def _load():
     lib.oracle_dequantize_rows.restype = ctypes.c_int
     lib.oracle_matmul_f16.argtypes = [p, i64, i64, p, i64, p]
     lib.oracle_matmul_f16.restype = ctypes.c_int
+    lib.oracle_backward.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p, p]
+    lib.oracle_backward.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_threads.argtypes = [ctypes.c_int]
@@ -161,3 +163,24 @@ def aqlm_matmul(codes, codebooks, scales, x, g: int = 8) -> np.ndarray:
     """Reference Y[t, i] = sum_c W[i, c] x[t, c] in fp64 with W = dequantize(...); [n, d_out]."""
     return matmul_f16(dequantize(codes, codebooks, scales, g), x)
 
+
+def backward(codes, codebooks, scales, x, dy, g: int = 8):
+    """Gradients through Eq. 2 for y = x W^T and an upstream gradient dy [n, d_out]:
+    returns (dcodebooks [M, 2^B, g], dscales [d_out]) in fp64, with
+    G = dy^T x, dC_m[e, k] = sum over (i, j) coded e in codebook m of s_i G[i, j g + k]
+    and ds_i = sum_c G[i, c] u[i, c] (u the fp32 codeword sums)."""
+    codes, cb, sc, d_out, d_in, M, B = _layer_args(codes, codebooks, scales, g)
+    xb = _bits16(x)
+    db = _bits16(dy)
+    if xb.ndim == 1:
+        xb = xb[None, :]
+    if db.ndim == 1:
+        db = db[None, :]
+    n = xb.shape[0]
+    if xb.shape != (n, d_in) or db.shape != (n, d_out):
+        raise ValueError("x must be [n, d_in] and dy [n, d_out]")
+    dcb = np.empty((M, 1 << B, g), dtype=np.float64)
+    ds = np.empty(d_out, dtype=np.float64)
+    _check(_load().oracle_backward(_ptr(codes), _ptr(cb), _ptr(sc), d_out, d_in, M, B, g, n, _ptr(xb), _ptr(db),
+                                   _ptr(dcb), _ptr(ds)))
+    return dcb, ds

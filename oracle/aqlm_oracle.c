@@ -210,6 +210,57 @@ int oracle_matmul_f16(const uint16_t* w, int64_t d_out, int64_t d_in, const uint
   return ORC_OK;
 }
 
+/* ---- gradients through Eq. 2 (the codebook and scale updates of Sec. 3,
+ * "Phase 2" and "Phase 3", and end-to-end fine-tuning) ----
+ *
+ * For y[t][i] = sum_c W[i][c] x[t][c] with W given by Eq. 2 and the scales
+ * (W[i][j*g + k] = s_i * u[i][j*g + k], u the sum over m of codeword
+ * b[i][j][m] of codebook m), and an upstream gradient dy = dL/dy, the chain
+ * rule gives, with G[i][c] = dL/dW[i][c] = sum_t dy[t][i] x[t][c]:
+ *   dL/dC_m[e][k] = sum over (i, j) with b[i][j][m] = e of s_i * G[i][j*g + k]
+ *   dL/ds_i       = sum_c G[i][c] * u[i][c]
+ * u is the fp32 sum of the codewords in ascending m (the sum the weights are
+ * rounded from; the rounding itself is not differentiated).  Everything else
+ * is fp64: G sums over t ascending, then i and c ascending.  dcodebooks is
+ * [M][2^B][g], dscales [d_out]; both are written (not accumulated). */
+int oracle_backward(const void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                    int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n,
+                    const uint16_t* x, const uint16_t* dy, double* dcodebooks, double* dscales) {
+  int st = check_args(codes, codebooks, scales, d_out, d_in, M, B, g);
+  if (st != ORC_OK) return st;
+  if (!x || !dy || !dcodebooks || !dscales) return ORC_ERR_NULL;
+  if (n <= 0) return ORC_ERR_SHAPE;
+  const int64_t groups = d_in / g;
+  const int64_t entries = (int64_t)1 << B;
+  const int64_t ncb = (int64_t)M * entries * g;
+  for (int64_t e = 0; e < ncb; ++e) dcodebooks[e] = 0.0;
+  for (int64_t i = 0; i < d_out; ++i) {
+    const double s = (double)oracle_f16_to_f32(scales[i]);
+    double ds = 0.0;
+    for (int64_t j = 0; j < groups; ++j) {
+      const int64_t code_base = (i * groups + j) * M;
+      for (int32_t m = 0; m < M; ++m)
+        if ((int64_t)code_at(codes, B, code_base + m) >= entries) return ORC_ERR_CODE;
+      for (int32_t k = 0; k < g; ++k) {
+        const int64_t c = j * g + k;
+        double G = 0.0;
+        for (int64_t t = 0; t < n; ++t)
+          G = G + (double)oracle_f16_to_f32(dy[t * d_out + i]) * (double)oracle_f16_to_f32(x[t * d_in + c]);
+        float u = 0.0f;
+        for (int32_t m = 0; m < M; ++m) {
+          const uint32_t b = code_at(codes, B, code_base + m);
+          const float v = oracle_f16_to_f32(codebooks[((int64_t)m * entries + b) * g + k]);
+          u = (m == 0) ? v : u + v;
+          dcodebooks[((int64_t)m * entries + b) * g + k] += s * G;
+        }
+        ds = ds + G * (double)u;
+      }
+    }
+    dscales[i] = ds;
+  }
+  return ORC_OK;
+}
+
 #ifdef _OPENMP
 #include <omp.h>
 #endif

@@ -345,3 +345,87 @@ def test_size_formula_worked_example_and_printed_bitwidths():
         assert round(bits, e["decimals"]) == e["bits"], e
     for e in gold["whole_model"]:
         assert round(fmt.model_bits_per_param(e["model"], e["M"], e["B"]), 2) == e["bits"], e
+
+
+# ------------------------------------------------------ gradients through Eq. 2
+
+def _loss_fp64(codes, cb, scales, x, dy):
+    """<dy, x W^T> with W = s * (sum of codewords) in exact fp64 arithmetic
+    (the loss whose gradient the backward pass computes, for a linear probe)."""
+    d_out, G, M = codes.shape
+    cbd = cb.astype(np.float64)
+    u = sum(cbd[m][codes[:, :, m].astype(np.int64)] for m in range(M)).reshape(d_out, G * 8)
+    w = scales.astype(np.float64)[:, None] * u
+    return float(np.sum((x.astype(np.float64) @ w.T) * dy.astype(np.float64)))
+
+
+@pytest.mark.parametrize("M,B", [(1, 8), (2, 8), (3, 4), (2, 12)])
+def test_backward_matches_autograd(M, B):
+    """torch autograd through the forward definition (fp64), an independent
+    route to the same gradients."""
+    torch = pytest.importorskip("torch")
+    lay = synth.layer(40 + M + B, 12, 48, M, B, n=5)
+    dy = np.random.default_rng(41).standard_normal((5, 12)).astype(np.float16)
+    dcb, ds = oracle.backward(lay.codes, lay.codebooks, lay.scales, lay.x, dy)
+    C = torch.tensor(lay.codebooks.astype(np.float64), requires_grad=True)
+    s = torch.tensor(lay.scales.astype(np.float64), requires_grad=True)
+    codes = torch.tensor(lay.codes.astype(np.int64))
+    u = sum(C[m][codes[:, :, m]] for m in range(M)).reshape(12, 48)
+    w = s[:, None] * u
+    y = torch.tensor(lay.x.astype(np.float64)) @ w.T
+    (y * torch.tensor(dy.astype(np.float64))).sum().backward()
+    np.testing.assert_allclose(dcb, C.grad.numpy(), rtol=1e-6, atol=1e-9)
+    np.testing.assert_allclose(ds, s.grad.numpy(), rtol=1e-6, atol=1e-9)
+
+
+def test_backward_finite_differences():
+    """The loss is linear in each codebook entry and each scale, so a central
+    difference equals the derivative up to fp64 rounding."""
+    lay = synth.layer(43, 10, 40, 2, 8, n=4)
+    dy = np.random.default_rng(44).standard_normal((4, 10)).astype(np.float16)
+    dcb, ds = oracle.backward(lay.codes, lay.codebooks, lay.scales, lay.x, dy)
+    rng = np.random.default_rng(45)
+    used = np.unique(lay.codes[:, :, 1])
+    for m, e, k in [(0, int(lay.codes[3, 2, 0]), 5), (1, int(used[0]), 0), (1, int(rng.integers(0, 256)), 7)]:
+        h = 0.5
+        cp, cm = lay.codebooks.astype(np.float64), lay.codebooks.astype(np.float64)
+        cp[m, e, k] += h
+        cm[m, e, k] -= h
+        fd = (_loss_fp64(lay.codes, cp, lay.scales, lay.x, dy) - _loss_fp64(lay.codes, cm, lay.scales, lay.x, dy)) / (2 * h)
+        assert abs(fd - dcb[m, e, k]) <= 1e-9 * max(1.0, abs(fd)), (m, e, k, fd, dcb[m, e, k])
+    for i in (0, 7):
+        sp, sm = lay.scales.astype(np.float64), lay.scales.astype(np.float64)
+        sp[i] += 0.25
+        sm[i] -= 0.25
+        fd = (_loss_fp64(lay.codes, lay.codebooks, sp, lay.x, dy) - _loss_fp64(lay.codes, lay.codebooks, sm, lay.x, dy)) / 0.5
+        assert abs(fd - ds[i]) <= 1e-6 * max(1.0, abs(fd))
+
+
+def test_backward_one_hot_upstream_closed_form():
+    """dy = one-hot at (token t, row i): G = e_i x_t^T, so codebook m's entry
+    e gets s_i * x_t[8j + k] for every group j of row i coded e, every other
+    row contributes nothing, and ds_i = sum_c x_t[c] u[i, c]."""
+    lay = synth.layer(46, 9, 64, 2, 8, n=3)
+    t, i = 2, 5
+    dy = np.zeros((3, 9), np.float16)
+    dy[t, i] = 1.0
+    dcb, ds = oracle.backward(lay.codes, lay.codebooks, lay.scales, lay.x, dy)
+    xt = lay.x[t].astype(np.float64)
+    s = float(lay.scales[i])
+    expect = np.zeros_like(dcb)
+    for j in range(8):
+        for m in range(2):
+            expect[m, lay.codes[i, j, m]] += s * xt[8 * j:8 * j + 8]
+    np.testing.assert_allclose(dcb, expect, rtol=0, atol=1e-12)
+    u = (lay.codebooks[0][lay.codes[i, :, 0]].astype(np.float32)
+         + lay.codebooks[1][lay.codes[i, :, 1]].astype(np.float32)).reshape(-1).astype(np.float64)
+    assert abs(ds[i] - math.fsum(xt * u)) <= 1e-12
+    assert np.all(ds[np.arange(9) != i] == 0)
+
+
+def test_backward_zero_upstream_and_errors():
+    lay = synth.layer(47, 4, 16, 2, 8, n=2)
+    dcb, ds = oracle.backward(lay.codes, lay.codebooks, lay.scales, lay.x, np.zeros((2, 4), np.float16))
+    assert not dcb.any() and not ds.any()
+    with pytest.raises(ValueError):
+        oracle.backward(lay.codes, lay.codebooks, lay.scales, lay.x, np.zeros((3, 4), np.float16))
