@@ -27,8 +27,8 @@ Also reported on the same JSON line:
                 with the CPU model and a one-thread time;
   secondary     the Llama-2-7B steps in 2x8 and 1x16, single layers rotated
                 over >= 1 GiB of replicas (so HBM, not the 256 MB MALL, is
-                measured), the small-batch / prefill products and
-                dequantization.
+                measured), the small-batch / prefill products,
+                dequantization and the gradients through Eq. 2.
 
 The timed region is bracketed by two short spin kernels outside its events,
 so that ``--summarize-trace`` can pick its dispatches out of a rocprofv3
@@ -82,6 +82,8 @@ def parse_args():
     ap.add_argument("--compare-paths", action="store_true",
                     help="only time the batch-1 2x8 launches of the Llama-2-70B step (and a 65536x8192 layer) "
                          "through both kernel families (codeword gathers, partial-product tables) and exit")
+    ap.add_argument("--backward", action="store_true",
+                    help="only time the gradients through Eq. 2 (aqlm_backward) and exit")
     ap.add_argument("--once", action="store_true",
                     help="with --compare-paths: launch each family once per case, untimed (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -455,6 +457,28 @@ def batch_rows(aq, torch, cases=None):
     return rows
 
 
+def backward_rows(aq, torch):
+    """Gradients through Eq. 2 (aqlm_backward) for 2x8 and 4x8 layers of
+    Llama-2-7B shapes: the weight-gradient contraction (2 n d_out d_in flops)
+    on the matrix cores plus the scatter into the codebook and scale
+    gradients."""
+    from paper_2401_06118_amd import format as fmt
+    rows = []
+    for d_out, d_in, M, n in ((11008, 4096, 2, 256), (11008, 4096, 2, 2048), (4096, 11008, 4, 2048)):
+        L = DeviceLayer(500000 + n + M, d_out, d_in, M, 8, n=n)
+        dy = torch.randn((n, d_out), device="cuda").half()
+        dcb = torch.zeros(tuple(L.codebooks.shape), dtype=torch.float32, device="cuda")
+        ds = torch.zeros((d_out,), dtype=torch.float32, device="cuda")
+        ms = time_steps(lambda: aq.backward(L.codes, L.codebooks, L.scales, L.x, dy, dcodebooks=dcb, dscales=ds),
+                        steps=5, warmup=1)
+        fl = fmt.AqlmShape(d_out, d_in, M, 8).flops(n)
+        rows.append({"layer": f"{d_out}x{d_in} {M}x8", "n": n, "us": ms * 1e3, "TFLOPs": fl / (ms * 1e9),
+                     "mfma_frac": fl / (ms * 1e9) / MFMA_F16_PEAK_TFS})
+        del L, dy, dcb, ds
+        torch.cuda.empty_cache()
+    return rows
+
+
 def kernel_name(M: int, B: int) -> str:
     """Device kernel that serves a batch-1 product of this format."""
     if B == 8 and M in (1, 2, 4):
@@ -562,6 +586,9 @@ def main():
     from paper_2401_06118_amd import _lib
 
     _lib.load()  # fail loudly if the HIP library is missing
+    if args.backward:
+        print(json.dumps({"backward": backward_rows(aq, torch)}), flush=True)
+        return
     if args.compare_paths:
         print(json.dumps({"paths": compare_paths(aq, torch, once=args.once)}), flush=True)
         return
@@ -672,6 +699,8 @@ def main():
         log("single layers done")
         sec["batch"] = batch_rows(aq, torch)
         log("batch / dequantize done")
+        sec["backward"] = backward_rows(aq, torch)
+        log("backward done")
         result["secondary"] = sec
     if not args.no_cpu_baseline:
         layers = decode_step_layers(model, M, B, step_seed(M))

@@ -181,6 +181,27 @@ int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scal
               int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n,
               const uint16_t* x, uint16_t* y, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Gradients through Eq. 2 for fine-tuning codebooks and scales (Sec. 3,
+ * "Phase 2: Codebook update" and "Phase 3: Fine-tuning"; App. "End-to-end
+ * fine-tuning"): for y = x W^T over n activation rows x [n][d_in] and the
+ * upstream gradient dy = dL/dy [n][d_out] (fp16), with
+ * G[i][c] = sum_t dy[t][i] x[t][c] and u[i][c] the fp32 sum of the codewords
+ * of row i, group c / g (the sum the weights are rounded from; the rounding
+ * is not differentiated), ACCUMULATES
+ *   dcodebooks[m][e][k] += sum over (i, j) with b[i][j][m] = e of s_i * G[i][j*g + k]
+ *   dscales[i]          += sum_c G[i][c] * u[i][c]
+ * into fp32 device arrays [M][2^B][g] and [d_out] (zero them for a fresh
+ * gradient; leave them to accumulate micro-batches).  G is computed in fp32
+ * on the matrix cores and never stored; no workspace.  The additions use
+ * atomics, so results agree with an exact computation to fp32 accuracy but
+ * may differ in the last bits from run to run.  Supported: B = 8 with
+ * 1 <= M <= 8, g = 8, d_out a multiple of 8 (else AQLM_ERR_UNSUPPORTED /
+ * AQLM_ERR_SHAPE); x and dy 16-byte aligned, the gradients 4-byte aligned.
+ * Other errors as aqlm_gemm_small_batch. */
+int aqlm_backward(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                  int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, const uint16_t* dy,
+                  float* dcodebooks, float* dscales, void* stream);
+
 /* Bytes of the fixed device scratch buffer of aqlm_gemm_noalloc (128 MiB). */
 #define AQLM_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
 

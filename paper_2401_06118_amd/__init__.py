@@ -10,7 +10,8 @@ Eq. 2 and Fig. 3).  This package exposes the three operations of the C ABI in
 - :func:`gemv_grouped` - several independent matrix-vector products in one launch;
 - :func:`gemm_small_batch` - the same product for n activation rows;
 - :func:`gemm` - that product with a workspace: for many rows the weights are
-  dequantized once, then a dense fp16 matrix-core product reads them.
+  dequantized once, then a dense fp16 matrix-core product reads them;
+- :func:`backward` - gradients of the codebooks and scales through Eq. 2.
 
 Every computation runs in the hand-written HIP kernels of
 ``libaqlm_mi355x.so``; this module only marshals arguments.
@@ -26,7 +27,8 @@ import torch
 from . import _lib
 from ._lib import AqlmError, status_string  # noqa: F401
 
-__all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "gemm_workspace_bytes", "gemm", "AqlmError",
+__all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "gemm_workspace_bytes", "gemm", "backward",
+           "AqlmError",
            "status_string", "layer_args"]
 
 
@@ -173,3 +175,30 @@ def gemm(codes, codebooks, scales, x, *, workspace=None, out=None, stream=None) 
                                x.data_ptr(), out.data_ptr(), ws_ptr, ws_bytes, _stream_handle(stream))
     _check(st, "aqlm_gemm")
     return out
+
+
+def backward(codes, codebooks, scales, x, dy, *, dcodebooks=None, dscales=None, stream=None):
+    """Gradients through Eq. 2 for y = x W^T: accumulates dL/dC into
+    ``dcodebooks`` (fp32 [M, 2^B, g]) and dL/ds into ``dscales`` (fp32 [d_out]),
+    new zero tensors when not given; returns (dcodebooks, dscales).  x [n, d_in]
+    and dy = dL/dy [n, d_out] are fp16."""
+    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    for name, t, shape in (("x", x, (None, d_in)), ("dy", dy, (None, d_out))):
+        if t.dtype != torch.float16 or t.dim() != 2 or t.shape[1] != shape[1] or not t.is_cuda \
+                or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp16 GPU tensor [n, {shape[1]}]")
+    n = x.shape[0]
+    if dy.shape[0] != n:
+        raise ValueError("x and dy must have the same number of rows")
+    if dcodebooks is None:
+        dcodebooks = torch.zeros(tuple(codebooks.shape), dtype=torch.float32, device=codes.device)
+    if dscales is None:
+        dscales = torch.zeros((d_out,), dtype=torch.float32, device=codes.device)
+    for name, t, shape in (("dcodebooks", dcodebooks, tuple(codebooks.shape)), ("dscales", dscales, (d_out,))):
+        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp32 GPU tensor of shape {shape}")
+    st = _lib.load().aqlm_backward(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in, M, B, g,
+                                   n, x.data_ptr(), dy.data_ptr(), dcodebooks.data_ptr(), dscales.data_ptr(),
+                                   _stream_handle(stream))
+    _check(st, "aqlm_backward")
+    return dcodebooks, dscales

@@ -250,6 +250,21 @@ int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scal
   return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, L.d_out, L.d_in, s));
 }
 
+int aqlm_backward(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                  int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, const uint16_t* dy,
+                  float* dcodebooks, float* dscales, void* stream) {
+  aqlm::Layer L;
+  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  if (!x || !dy || !dcodebooks || !dscales) return AQLM_ERR_NULL;
+  if (n <= 0 || n >= (int64_t(1) << 31) || n * d_in >= (int64_t(1) << 40) || n * d_out >= (int64_t(1) << 40))
+    return AQLM_ERR_SHAPE;
+  if (B != 8) return AQLM_ERR_UNSUPPORTED;
+  if (d_out % 8 != 0) return AQLM_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(dy, 16) || !aligned(dcodebooks, 4) || !aligned(dscales, 4)) return AQLM_ERR_ALIGN;
+  return status_of(aqlm::launch_backward(L, (int32_t)n, x, dy, dcodebooks, dscales, static_cast<hipStream_t>(stream)));
+}
+
 int aqlm_gemm_noalloc(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                       int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
                       void* stream) {

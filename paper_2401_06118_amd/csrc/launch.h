@@ -77,6 +77,12 @@ size_t gemm_f16_part_bytes(int64_t n, int64_t d_out, int64_t K);
 hipError_t launch_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, float* part, int32_t n, int32_t d_out,
                            int32_t K, hipStream_t s);
 
+// Gradients through Eq. 2 (8-bit codes, d_out a multiple of 8): accumulates
+// dC and dscales for y = x W^T and an upstream gradient dy.
+bool backward_supported(const Layer& L);
+hipError_t launch_backward(const Layer& L, int32_t n, const uint16_t* x, const uint16_t* dy, float* dcb, float* ds,
+                           hipStream_t s);
+
 int num_cus();
 // Allows a kernel `bytes` of dynamic LDS on the current device (once per
 // kernel, device and size).

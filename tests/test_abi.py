@@ -192,3 +192,16 @@ def test_noalloc_refuses_before_launch(lib):
     assert call(d_out=12288, d_in=8192) == 7            # 192 MiB of weights
     assert call(d_out=28672, d_in=8192, n=2048) == 7
     assert lib.aqlm_status_string(7) != b"unknown status"
+
+
+def test_backward_refuses_before_launch(lib):
+    def call(codes=P, d_out=64, d_in=64, M=2, B=8, n=4, x=P, dy=P, dc=P, ds=P):
+        return lib.aqlm_backward(codes, P, P, d_out, d_in, M, B, 8, n, x, dy, dc, ds, None)
+    assert call(dc=None) == NULL
+    assert call(dy=None) == NULL
+    assert call(n=0) == SHAPE
+    assert call(d_out=60) == SHAPE          # d_out not a multiple of 8
+    assert call(M=1, B=16) == UNSUP
+    assert call(M=2, B=12) == UNSUP
+    assert call(dy=P + 2) == ALIGN
+    assert call(ds=P + 2) == ALIGN

@@ -671,6 +671,64 @@ def test_gemm_random_shapes(seed):
     check_products(lay, fp16_to_np(y2))
 
 
+# ------------------------------------------------- gradients through Eq. 2
+
+BACKWARD_CASES = [
+    # (d_out, d_in, M, n)
+    (64, 256, 2, 32),
+    (200, 520, 1, 37),       # ragged tokens and inputs, d_out not a multiple of 128
+    (1000, 1040, 4, 64),
+    (1024, 4096, 2, 128),    # Llama-2-7B input width
+    (96, 384, 3, 5), (40, 128, 5, 9), (16, 64, 6, 1), (8, 8, 7, 3), (136, 264, 8, 70),
+]
+
+
+def _backward_check(lay, dy, dcb, ds):
+    ref_cb, ref_ds = oracle.backward(lay.codes, lay.codebooks, lay.scales, lay.x, dy)
+    got_cb = dcb.double().cpu().numpy()
+    got_ds = ds.double().cpu().numpy()
+    assert rel_l2(got_cb, ref_cb) <= 1e-4, rel_l2(got_cb, ref_cb)
+    assert rel_l2(got_ds, ref_ds) <= 1e-4, rel_l2(got_ds, ref_ds)
+    assert np.max(np.abs(got_cb - ref_cb)) <= 1e-4 * np.max(np.abs(ref_cb))
+    assert np.max(np.abs(got_ds - ref_ds)) <= 1e-4 * np.max(np.abs(ref_ds))
+
+
+@pytest.mark.parametrize("d_out,d_in,M,n", BACKWARD_CASES)
+def test_backward_matches_oracle(d_out, d_in, M, n):
+    print(f"[backward] d_out={d_out} d_in={d_in} M={M} n={n}", flush=True)
+    lay = synth.layer(20000 + d_out + d_in + M, d_out, d_in, M, 8, n=n)
+    dy = np.random.default_rng(20001 + n).standard_normal((n, d_out)).astype(np.float16)
+    codes, cb, sc, x = to_device(lay)
+    dcb, ds = aq().backward(codes, cb, sc, x, torch.from_numpy(dy).cuda())
+    torch.cuda.synchronize()
+    _backward_check(lay, dy, dcb, ds)
+
+
+def test_backward_accumulates_and_cancelling():
+    """Two calls add up (micro-batch accumulation); codebooks that cancel in
+    pairs give the same gradients as the oracle."""
+    lay = synth.cancelling_layer(20100, 256, 512, 4, n=48)
+    dy = np.random.default_rng(20101).standard_normal((48, 256)).astype(np.float16)
+    codes, cb, sc, x = to_device(lay)
+    dyt = torch.from_numpy(dy).cuda()
+    dcb, ds = aq().backward(codes, cb, sc, x, dyt)
+    aq().backward(codes, cb, sc, x, dyt, dcodebooks=dcb, dscales=ds)
+    torch.cuda.synchronize()
+    _backward_check(lay, dy, dcb / 2, ds / 2)
+
+
+def test_backward_refuses_before_launch():
+    lay = synth.layer(20200, 64, 256, 2, 8, n=4)
+    codes, cb, sc, x = to_device(lay)
+    dy = torch.zeros((4, 64), dtype=torch.float16, device="cuda")
+    with pytest.raises(ValueError):
+        aq().backward(codes, cb, sc, x, dy[:3])
+    lay16 = synth.layer(20201, 64, 256, 1, 16, n=4)
+    c16, cb16, sc16, x16 = to_device(lay16)
+    with pytest.raises(aq().AqlmError):
+        aq().backward(c16, cb16, sc16, x16, dy)
+
+
 # -------------------------------------------------- 1x15 (15-bit codes)
 
 @pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (11008, 4096), (4096, 11008), (1000, 4104), (37, 8)])
