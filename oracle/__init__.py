@@ -55,6 +55,10 @@ def _load():
     lib.oracle_matmul_f16.restype = ctypes.c_int
     lib.oracle_backward.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p, p]
     lib.oracle_backward.restype = ctypes.c_int
+    lib.oracle_aq_loss.argtypes = [p, p, p, p, p, i64, i64, i32, i32, i32, p]
+    lib.oracle_aq_loss.restype = ctypes.c_int
+    lib.oracle_beam_search.argtypes = [p, p, p, p, p, i64, i64, i32, i32, i32, i32, i32, p]
+    lib.oracle_beam_search.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_threads.argtypes = [ctypes.c_int]
@@ -184,3 +188,34 @@ def backward(codes, codebooks, scales, x, dy, g: int = 8):
     _check(_load().oracle_backward(_ptr(codes), _ptr(cb), _ptr(sc), d_out, d_in, M, B, g, n, _ptr(xb), _ptr(db),
                                    _ptr(dcb), _ptr(ds)))
     return dcb, ds
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+
+
+def aq_loss(w, h, codes, codebooks, scales, g: int = 8) -> np.ndarray:
+    """Per-row objective (w_i - what_i) H (w_i - what_i)^T in fp64, what the exact
+    (unrounded) reconstruction of Eq. 2 with scales; w [d_out, d_in], H [d_in, d_in]."""
+    codes, cb, sc, d_out, d_in, M, B = _layer_args(codes, codebooks, scales, g)
+    wf, hf = _f32(w), _f32(h)
+    if wf.shape != (d_out, d_in) or hf.shape != (d_in, d_in):
+        raise ValueError("w must be [d_out, d_in] and h [d_in, d_in]")
+    out = np.empty(d_out, dtype=np.float64)
+    _check(_load().oracle_aq_loss(_ptr(wf), _ptr(hf), _ptr(codes), _ptr(cb), _ptr(sc), d_out, d_in, M, B, g,
+                                  _ptr(out)))
+    return out
+
+
+def beam_search(w, h, codes, codebooks, scales, beam: int, sweeps: int = 1, g: int = 8):
+    """Phase-1 beam search over codes (fp64); returns (new codes, per-row loss).
+    See aqlm_oracle.c for the step order and tie rules."""
+    codes, cb, sc, d_out, d_in, M, B = _layer_args(codes, codebooks, scales, g)
+    wf, hf = _f32(w), _f32(h)
+    if wf.shape != (d_out, d_in) or hf.shape != (d_in, d_in):
+        raise ValueError("w must be [d_out, d_in] and h [d_in, d_in]")
+    out = codes.copy()
+    loss = np.empty(d_out, dtype=np.float64)
+    _check(_load().oracle_beam_search(_ptr(wf), _ptr(hf), _ptr(out), _ptr(cb), _ptr(sc), d_out, d_in, M, B, g,
+                                      int(beam), int(sweeps), _ptr(loss)))
+    return out, loss

@@ -33,6 +33,7 @@
  * (M, B, g), 4 a code outside [0, 2^B).
  */
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #define ORC_OK 0
@@ -259,6 +260,205 @@ int oracle_backward(const void* codes, const uint16_t* codebooks, const uint16_t
     dscales[i] = ds;
   }
   return ORC_OK;
+}
+
+/* ---- Phase 1: beam search over codes (Sec. 3, "Phase 1: Beam search for
+ * codes"; the codes step of the algorithm listing) ----
+ *
+ * Row i's objective is the squared error of Eq. main_obj restricted to that
+ * row, written with H = X X^T as in Eq. obj_mrf:
+ *   L_i(b) = (w_i - what_i) H (w_i - what_i)^T,
+ *   what_i[j*g + t] = s_i * sum_m C_m[b_ijm][t]   (exact, no fp16 rounding).
+ * Rows are independent.  A beam of at most k configurations of the row's
+ * codes starts as the current codes alone.  One step takes one code position
+ * (j, m) - positions are swept group by group, codebooks in ascending order
+ * within a group - and tries, for every configuration of the beam, every
+ * codeword e of codebook m at that position; the beam becomes the k
+ * distinct configurations of least loss among those candidates (ties: the
+ * earlier beam entry, then the smaller e).  Setting a position to its current
+ * code keeps a configuration, so the best loss never increases.  A
+ * candidate's loss is the previous loss plus the change of the terms that
+ * involve group j: with r = w - what and delta = s (C_m[e] - C_m[b_ijm]) on
+ * group j's g coordinates,
+ *   L' = L - 2 delta . (H r)_j + delta H_jj delta^T.
+ * H r is recomputed from r for every configuration at every step.  After
+ * `sweeps` sweeps the best configuration is the result.  Everything in fp64
+ * (W, H, codebooks and scales as given).  codes is read and overwritten;
+ * loss_out[i] receives the final loss of row i. */
+
+typedef struct {
+  double score;
+  int32_t beam;
+  int32_t code;
+} orc_cand;
+
+static int orc_cand_cmp(const void* pa, const void* pb) {
+  const orc_cand* a = (const orc_cand*)pa;
+  const orc_cand* b = (const orc_cand*)pb;
+  if (a->score < b->score) return -1;
+  if (a->score > b->score) return 1;
+  if (a->beam != b->beam) return a->beam < b->beam ? -1 : 1;
+  return a->code < b->code ? -1 : (a->code > b->code ? 1 : 0);
+}
+
+static void set_code(void* codes, int32_t B, int64_t idx, uint32_t v) {
+  if (B <= 8)
+    ((uint8_t*)codes)[idx] = (uint8_t)v;
+  else
+    ((uint16_t*)codes)[idx] = (uint16_t)v;
+}
+
+/* The loss of row i of the given codes: (w - what) H (w - what)^T in fp64. */
+static double row_loss(const float* w_row, const float* h, const void* codes_row, const uint16_t* codebooks,
+                       double s, int64_t d_in, int32_t M, int32_t B, int32_t g, double* r) {
+  const int64_t groups = d_in / g;
+  const int64_t entries = (int64_t)1 << B;
+  for (int64_t j = 0; j < groups; ++j)
+    for (int32_t t = 0; t < g; ++t) {
+      double u = 0.0;
+      for (int32_t m = 0; m < M; ++m) {
+        const uint32_t b = code_at(codes_row, B, j * M + m);
+        u += (double)oracle_f16_to_f32(codebooks[((int64_t)m * entries + b) * g + t]);
+      }
+      r[j * g + t] = (double)w_row[j * g + t] - s * u;
+    }
+  double loss = 0.0;
+  for (int64_t a = 0; a < d_in; ++a) {
+    double hr = 0.0;
+    for (int64_t c = 0; c < d_in; ++c) hr += (double)h[a * d_in + c] * r[c];
+    loss += r[a] * hr;
+  }
+  return loss;
+}
+
+int oracle_aq_loss(const float* w, const float* h, const void* codes, const uint16_t* codebooks,
+                   const uint16_t* scales, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                   double* loss_out) {
+  int st = check_args(codes, codebooks, scales, d_out, d_in, M, B, g);
+  if (st != ORC_OK) return st;
+  if (!w || !h || !loss_out) return ORC_ERR_NULL;
+  const int64_t groups = d_in / g;
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+  for (int64_t i = 0; i < d_out; ++i) {
+    double* r = (double*)malloc(sizeof(double) * d_in);
+    if (!r) { bad = 1; continue; }
+    const void* row = (B <= 8) ? (const void*)((const uint8_t*)codes + i * groups * M)
+                               : (const void*)((const uint16_t*)codes + i * groups * M);
+    loss_out[i] = row_loss(w + i * d_in, h, row, codebooks, (double)oracle_f16_to_f32(scales[i]), d_in, M, B, g, r);
+    free(r);
+  }
+  return bad ? ORC_ERR_NULL : ORC_OK;
+}
+
+int oracle_beam_search(const float* w, const float* h, void* codes, const uint16_t* codebooks,
+                       const uint16_t* scales, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                       int32_t beam, int32_t sweeps, double* loss_out) {
+  int st = check_args(codes, codebooks, scales, d_out, d_in, M, B, g);
+  if (st != ORC_OK) return st;
+  if (!w || !h || !loss_out) return ORC_ERR_NULL;
+  if (beam < 1 || sweeps < 0) return ORC_ERR_SHAPE;
+  if (g > 64) return ORC_ERR_UNSUPPORTED;
+  const int64_t groups = d_in / g;
+  const int64_t entries = (int64_t)1 << B;
+  const int64_t ncodes = groups * M;
+  const size_t cb = (B <= 8) ? 1 : 2;
+  for (int64_t e = 0; e < d_out * ncodes; ++e)
+    if ((int64_t)code_at(codes, B, e) >= entries) return ORC_ERR_CODE;
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+  for (int64_t i = 0; i < d_out; ++i) {
+    const double s = (double)oracle_f16_to_f32(scales[i]);
+    const float* w_row = w + i * d_in;
+    void* out_row = (char*)codes + (size_t)(i * ncodes) * cb;
+    /* beam state: codes, residual r = w - what, loss; two generations */
+    unsigned char* bc[2];
+    double* br[2];
+    double* bl[2];
+    double* hr = (double*)malloc(sizeof(double) * d_in);
+    orc_cand* cand = (orc_cand*)malloc(sizeof(orc_cand) * (size_t)(beam * entries));
+    int ok = hr && cand;
+    for (int q = 0; q < 2; ++q) {
+      bc[q] = (unsigned char*)malloc((size_t)(beam * ncodes) * cb);
+      br[q] = (double*)malloc(sizeof(double) * (size_t)(beam * d_in));
+      bl[q] = (double*)malloc(sizeof(double) * (size_t)beam);
+      ok = ok && bc[q] && br[q] && bl[q];
+    }
+    if (!ok) {
+      bad = 1;
+    } else {
+      int cur = 0, nb = 1;
+      memcpy(bc[0], out_row, (size_t)ncodes * cb);
+      bl[0][0] = row_loss(w_row, h, bc[0], codebooks, s, d_in, M, B, g, br[0]);
+      for (int32_t sw = 0; sw < sweeps; ++sw)
+        for (int64_t j = 0; j < groups; ++j)
+          for (int32_t m = 0; m < M; ++m) {
+            const int64_t pos = j * M + m;
+            int nc = 0;
+            for (int b = 0; b < nb; ++b) {
+              const unsigned char* cfg = bc[cur] + (size_t)(b * ncodes) * cb;
+              const double* r = br[cur] + (size_t)b * d_in;
+              for (int32_t t = 0; t < g; ++t) {
+                double acc = 0.0;
+                for (int64_t c = 0; c < d_in; ++c) acc += (double)h[(j * g + t) * d_in + c] * r[c];
+                hr[j * g + t] = acc;
+              }
+              const uint32_t o = code_at(cfg, B, pos);
+              for (int64_t e = 0; e < entries; ++e) {
+                double delta[64];
+                for (int32_t t = 0; t < g; ++t)
+                  delta[t] = s * ((double)oracle_f16_to_f32(codebooks[((int64_t)m * entries + e) * g + t]) -
+                                  (double)oracle_f16_to_f32(codebooks[((int64_t)m * entries + o) * g + t]));
+                double lin = 0.0, quad = 0.0;
+                for (int32_t t = 0; t < g; ++t) {
+                  lin += delta[t] * hr[j * g + t];
+                  double hd = 0.0;
+                  for (int32_t u = 0; u < g; ++u) hd += (double)h[(j * g + t) * d_in + j * g + u] * delta[u];
+                  quad += delta[t] * hd;
+                }
+                cand[nc].score = bl[cur][b] - 2.0 * lin + quad;
+                cand[nc].beam = b;
+                cand[nc].code = (int32_t)e;
+                ++nc;
+              }
+            }
+            qsort(cand, (size_t)nc, sizeof(orc_cand), orc_cand_cmp);
+            const int nxt = 1 - cur;
+            int nn = 0;
+            for (int q = 0; q < nc && nn < beam; ++q) {
+              unsigned char* dst = bc[nxt] + (size_t)(nn * ncodes) * cb;
+              memcpy(dst, bc[cur] + (size_t)(cand[q].beam * ncodes) * cb, (size_t)ncodes * cb);
+              set_code(dst, B, pos, (uint32_t)cand[q].code);
+              int dup = 0;
+              for (int p2 = 0; p2 < nn && !dup; ++p2)
+                dup = memcmp(dst, bc[nxt] + (size_t)(p2 * ncodes) * cb, (size_t)ncodes * cb) == 0;
+              if (dup) continue;
+              /* residual of the new configuration: only group j changes */
+              const double* rsrc = br[cur] + (size_t)cand[q].beam * d_in;
+              double* rdst = br[nxt] + (size_t)nn * d_in;
+              memcpy(rdst, rsrc, sizeof(double) * (size_t)d_in);
+              const uint32_t o = code_at(bc[cur] + (size_t)(cand[q].beam * ncodes) * cb, B, pos);
+              for (int32_t t = 0; t < g; ++t)
+                rdst[j * g + t] -= s * ((double)oracle_f16_to_f32(codebooks[((int64_t)m * entries + cand[q].code) * g + t]) -
+                                        (double)oracle_f16_to_f32(codebooks[((int64_t)m * entries + o) * g + t]));
+              bl[nxt][nn] = cand[q].score;
+              ++nn;
+            }
+            cur = nxt;
+            nb = nn;
+          }
+      memcpy(out_row, bc[cur], (size_t)ncodes * cb);
+      loss_out[i] = bl[cur][0];
+    }
+    for (int q = 0; q < 2; ++q) {
+      free(bc[q]);
+      free(br[q]);
+      free(bl[q]);
+    }
+    free(hr);
+    free(cand);
+  }
+  return bad ? ORC_ERR_NULL : ORC_OK;
 }
 
 #ifdef _OPENMP

@@ -429,3 +429,97 @@ def test_backward_zero_upstream_and_errors():
     assert not dcb.any() and not ds.any()
     with pytest.raises(ValueError):
         oracle.backward(lay.codes, lay.codebooks, lay.scales, lay.x, np.zeros((3, 4), np.float16))
+
+
+# --------------------------------------------------- Phase 1: beam search
+
+def _objective_x(w, x, codes, cb, scales):
+    """||(w - what) X||^2 per row, straight from Eq. main_obj with X itself
+    (not X X^T): an independent route to the objective the search minimises."""
+    d_out, G, M = codes.shape
+    cbd = cb.astype(np.float64)
+    u = sum(cbd[m][codes[:, :, m].astype(np.int64)] for m in range(M)).reshape(d_out, G * 8)
+    what = scales.astype(np.float64)[:, None] * u
+    return np.sum(((w.astype(np.float64) - what) @ x.astype(np.float64)) ** 2, axis=1)
+
+
+def _beam_problem(seed, d_out, d_in, M, B, n_x=48, w_scale=0.05):
+    rng = np.random.default_rng(seed)
+    lay = synth.layer(seed, d_out, d_in, M, B)
+    # small integers, so that X X^T is exact in the fp32 the search is given
+    x = rng.integers(-3, 4, size=(d_in, n_x)).astype(np.float32)
+    h = (x.astype(np.float64) @ x.T.astype(np.float64)).astype(np.float32)
+    w = (rng.standard_normal((d_out, d_in)) * w_scale).astype(np.float32)
+    return lay, w, x, h
+
+
+@pytest.mark.parametrize("M,B,beam", [(2, 8, 4), (1, 8, 1), (3, 4, 2), (1, 10, 3)])
+def test_beam_search_loss_is_the_objective(M, B, beam):
+    """The search's own (incremental) losses equal ||(w - what) X||^2 of the codes it
+    returns, which never exceeds that of the codes it started from."""
+    lay, w, x, h = _beam_problem(50 + M + B, 12, 64, M, B)
+    before = _objective_x(w, x, lay.codes, lay.codebooks, lay.scales)
+    codes, loss = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=beam, sweeps=2)
+    after = _objective_x(w, x, codes, lay.codebooks, lay.scales)
+    np.testing.assert_allclose(loss, after, rtol=1e-9)
+    assert np.all(after <= before * (1 + 1e-12))
+    np.testing.assert_allclose(oracle.aq_loss(w, h, codes, lay.codebooks, lay.scales), after, rtol=1e-9)
+
+
+def test_beam_search_reaches_the_optimum_when_the_beam_holds_every_prefix():
+    """One group, two codebooks of 4 codewords, beam 4: after the first step the
+    beam holds all 4 choices of the first code, so the second step scores all
+    16 configurations and must return the best of them (brute force)."""
+    lay, w, x, h = _beam_problem(60, 16, 8, 2, 2)
+    codes, loss = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=4, sweeps=1)
+    for i in range(16):
+        best = None
+        for a in range(4):
+            for b in range(4):
+                c = np.array([[[a, b]]], np.uint8)
+                v = _objective_x(w[i:i + 1], x, c, lay.codebooks, lay.scales[i:i + 1])[0]
+                if best is None or v < best[0] - 1e-12:
+                    best = (v, a, b)
+        assert abs(loss[i] - best[0]) <= 1e-9 * best[0]
+        assert tuple(codes[i, 0]) == best[1:]
+
+
+def test_beam_search_identity_h_picks_nearest_codewords():
+    """H = I decouples the groups: with one codebook the search must give every
+    group its nearest scaled codeword, argmin_e ||w_j - s C_e||^2."""
+    lay, w, x, h = _beam_problem(61, 10, 40, 1, 8)
+    h = np.eye(40, dtype=np.float32)
+    codes, _ = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=1, sweeps=1)
+    cb = lay.codebooks[0].astype(np.float64)
+    for i in range(10):
+        s = float(lay.scales[i])
+        for j in range(5):
+            d = ((w[i, 8 * j:8 * j + 8].astype(np.float64)[None, :] - s * cb) ** 2).sum(axis=1)
+            assert codes[i, j, 0] == int(np.argmin(d))
+
+
+def test_beam_one_is_greedy_coordinate_descent():
+    """Beam 1: each step sets one code to the codeword of least objective given
+    the others (ties to the smaller index) - written here as a plain loop."""
+    lay, w, x, h = _beam_problem(62, 6, 32, 2, 4)
+    codes, _ = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=1, sweeps=2)
+    ref = lay.codes.copy()
+    for _ in range(2):
+        for j in range(4):
+            for m in range(2):
+                for i in range(6):
+                    vals = []
+                    for e in range(16):
+                        c = ref[i:i + 1].copy()
+                        c[0, j, m] = e
+                        vals.append(_objective_x(w[i:i + 1], x, c, lay.codebooks, lay.scales[i:i + 1])[0])
+                    vals = np.array(vals)
+                    ref[i, j, m] = int(np.flatnonzero(vals <= vals.min() * (1 + 1e-12))[0])
+    assert np.array_equal(codes, ref)
+
+
+def test_beam_search_more_sweeps_never_worse():
+    lay, w, x, h = _beam_problem(63, 8, 48, 2, 6)
+    _, l1 = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=3, sweeps=1)
+    _, l3 = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=3, sweeps=3)
+    assert np.all(l3 <= l1 * (1 + 1e-12))
