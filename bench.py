@@ -28,7 +28,8 @@ Also reported on the same JSON line:
   secondary     the Llama-2-7B steps in 2x8 and 1x16, single layers rotated
                 over >= 1 GiB of replicas (so HBM, not the 256 MB MALL, is
                 measured), the small-batch / prefill products,
-                dequantization and the gradients through Eq. 2.
+                dequantization, the gradients through Eq. 2 and the Phase-1
+                beam search.
 
 The timed region is bracketed by two short spin kernels outside its events,
 so that ``--summarize-trace`` can pick its dispatches out of a rocprofv3
@@ -84,6 +85,8 @@ def parse_args():
                          "through both kernel families (codeword gathers, partial-product tables) and exit")
     ap.add_argument("--backward", action="store_true",
                     help="only time the gradients through Eq. 2 (aqlm_backward) and exit")
+    ap.add_argument("--beam-search", action="store_true",
+                    help="only time the Phase-1 beam search (aqlm_beam_search) and exit")
     ap.add_argument("--once", action="store_true",
                     help="with --compare-paths: launch each family once per case, untimed (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -479,6 +482,36 @@ def backward_rows(aq, torch):
     return rows
 
 
+def beam_rows(aq, torch):
+    """Phase-1 beam search (aqlm_beam_search): one sweep over every code
+    position of 2x8 layers, H = X X^T from 512 random calibration vectors."""
+    rows = []
+    for d_out, d_in, M, beam in ((4096, 1024, 2, 4), (4096, 2048, 2, 8)):
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(400000 + d_in + beam)
+        x = torch.randn((d_in, 512), device="cuda", generator=gen)
+        h = (x @ x.T).contiguous()
+        w = (torch.randn((d_out, d_in), device="cuda", generator=gen) * 0.05).contiguous()
+        L = DeviceLayer(400000 + d_in, d_out, d_in, M, 8)
+        codes0 = L.codes.clone()
+        ms = []
+        for _ in range(2):
+            L.codes.copy_(codes0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            loss = aq.beam_search(w, h, L.codes, L.codebooks, L.scales, beam=beam, sweeps=1)
+            torch.cuda.synchronize()
+            ms.append((time.perf_counter() - t0) * 1e3)
+        steps = d_in // 8 * M
+        rows.append({"layer": f"{d_out}x{d_in} {M}x8", "beam": beam, "sweeps": 1, "ms": min(ms),
+                     "rows_per_s": d_out / (min(ms) / 1e3),
+                     "candidates_per_s": d_out * steps * beam * 256 / (min(ms) / 1e3),
+                     "mean_loss": float(loss.mean())})
+        del L, x, h, w
+        torch.cuda.empty_cache()
+    return rows
+
+
 def kernel_name(M: int, B: int) -> str:
     """Device kernel that serves a batch-1 product of this format."""
     if B == 8 and M in (1, 2, 4):
@@ -588,6 +621,9 @@ def main():
     _lib.load()  # fail loudly if the HIP library is missing
     if args.backward:
         print(json.dumps({"backward": backward_rows(aq, torch)}), flush=True)
+        return
+    if args.beam_search:
+        print(json.dumps({"beam_search": beam_rows(aq, torch)}), flush=True)
         return
     if args.compare_paths:
         print(json.dumps({"paths": compare_paths(aq, torch, once=args.once)}), flush=True)
@@ -701,6 +737,8 @@ def main():
         log("batch / dequantize done")
         sec["backward"] = backward_rows(aq, torch)
         log("backward done")
+        sec["beam_search"] = beam_rows(aq, torch)
+        log("beam search done")
         result["secondary"] = sec
     if not args.no_cpu_baseline:
         layers = decode_step_layers(model, M, B, step_seed(M))

@@ -202,6 +202,33 @@ int aqlm_backward(const void* codes, const uint16_t* codebooks, const uint16_t* 
                   int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, const uint16_t* dy,
                   float* dcodebooks, float* dscales, void* stream);
 
+/* Phase 1 of AQLM, beam search over the codes (Sec. 3, "Phase 1: Beam search
+ * for codes"): for every output row i, with H = X X^T [d_in][d_in] (fp32,
+ * symmetric) and the original weights w [d_out][d_in] (fp32), improves the
+ * row's codes for the objective
+ *   L_i = (w_i - what_i) H (w_i - what_i)^T,  what_i[8j + t] = s_i sum_m C_m[b_ijm][t]
+ * (the layer's squared output error over the calibration inputs X, Eq.
+ * main_obj; what is the exact reconstruction, not rounded to fp16).  A beam
+ * of at most `beam` configurations starts as the row's current codes; each
+ * step takes one code position (groups in ascending order, codebooks in
+ * ascending order within a group), tries every codeword there for every
+ * configuration in the beam, and keeps the `beam` distinct configurations of
+ * least loss (ties: earlier beam entry, then smaller code); `sweeps` passes
+ * over all positions; the best configuration is written back to `codes`
+ * (in place).  Candidate losses are the entry's loss plus a change computed
+ * incrementally in fp32 from H r and the H_jj block, as the paper describes
+ * (fp32 and exact arithmetic can break near-ties differently).  `loss_out`
+ * (fp32 [d_out], may be NULL) receives each row's final loss, recomputed
+ * exactly (fp64) from the returned codes.  Rows are searched in parallel (one
+ * workgroup per row, the beam state in on-chip memory).
+ * Supported: B = 8, 1 <= M <= 8, g = 8, 1 <= beam <= 8, and
+ * 8 * beam * d_in + 2 * beam * d_in / 8 * M + 4096 * M bytes of state within
+ * about 158 KiB (d_in up to 2048 with beam 8, 4096 with beam 4); otherwise
+ * AQLM_ERR_UNSUPPORTED.  w, h and loss_out 4-byte aligned.  Deterministic. */
+int aqlm_beam_search(const float* w, const float* h, void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                     int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int32_t beam, int32_t sweeps,
+                     float* loss_out, void* stream);
+
 /* Bytes of the fixed device scratch buffer of aqlm_gemm_noalloc (128 MiB). */
 #define AQLM_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
 

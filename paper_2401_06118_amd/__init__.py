@@ -11,7 +11,8 @@ Eq. 2 and Fig. 3).  This package exposes the three operations of the C ABI in
 - :func:`gemm_small_batch` - the same product for n activation rows;
 - :func:`gemm` - that product with a workspace: for many rows the weights are
   dequantized once, then a dense fp16 matrix-core product reads them;
-- :func:`backward` - gradients of the codebooks and scales through Eq. 2.
+- :func:`backward` - gradients of the codebooks and scales through Eq. 2;
+- :func:`beam_search` - Phase 1 of the quantizer: beam search over the codes.
 
 Every computation runs in the hand-written HIP kernels of
 ``libaqlm_mi355x.so``; this module only marshals arguments.
@@ -28,6 +29,7 @@ from . import _lib
 from ._lib import AqlmError, status_string  # noqa: F401
 
 __all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "gemm_workspace_bytes", "gemm", "backward",
+           "beam_search",
            "AqlmError",
            "status_string", "layer_args"]
 
@@ -202,3 +204,20 @@ def backward(codes, codebooks, scales, x, dy, *, dcodebooks=None, dscales=None, 
                                    _stream_handle(stream))
     _check(st, "aqlm_backward")
     return dcodebooks, dscales
+
+
+def beam_search(w, h, codes, codebooks, scales, *, beam: int, sweeps: int = 1, stream=None) -> torch.Tensor:
+    """Phase-1 beam search over the codes of every row for the objective
+    (w_i - what_i) H (w_i - what_i)^T, H = X X^T; ``codes`` (uint8 [d_out, d_in/8, M])
+    is improved in place.  w: fp32 [d_out, d_in]; h: fp32 [d_in, d_in].
+    Returns each row's final loss (fp32 [d_out])."""
+    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    for name, t, shape in (("w", w, (d_out, d_in)), ("h", h, (d_in, d_in))):
+        if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp32 GPU tensor of shape {shape}")
+    loss = torch.empty((d_out,), dtype=torch.float32, device=codes.device)
+    st = _lib.load().aqlm_beam_search(w.data_ptr(), h.data_ptr(), codes.data_ptr(), codebooks.data_ptr(),
+                                      scales.data_ptr(), d_out, d_in, M, B, g, int(beam), int(sweeps),
+                                      loss.data_ptr(), _stream_handle(stream))
+    _check(st, "aqlm_beam_search")
+    return loss

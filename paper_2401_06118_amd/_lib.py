@@ -19,7 +19,7 @@ STATUS_NAMES = {0: "AQLM_OK", 1: "AQLM_ERR_NULL", 2: "AQLM_ERR_SHAPE", 3: "AQLM_
                 4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP", 6: "AQLM_ERR_WORKSPACE", 7: "AQLM_ERR_SCRATCH"}
 PATH_AUTO, PATH_GATHER, PATH_TABLE = 0, 1, 2
 EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemv_grouped_path", "aqlm_gemm_small_batch",
-           "aqlm_gemm_workspace_bytes", "aqlm_gemm", "aqlm_gemm_noalloc", "aqlm_backward",
+           "aqlm_gemm_workspace_bytes", "aqlm_gemm", "aqlm_gemm_noalloc", "aqlm_backward", "aqlm_beam_search",
            "aqlm_status_string")
 MAX_GROUPED = 8
 
@@ -72,6 +72,8 @@ def load():
         lib.aqlm_gemm_noalloc.restype = ctypes.c_int
         lib.aqlm_backward.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p, p, p]
         lib.aqlm_backward.restype = ctypes.c_int
+        lib.aqlm_beam_search.argtypes = [p, p, p, p, p, i64, i64, i32, i32, i32, i32, i32, p, p]
+        lib.aqlm_beam_search.restype = ctypes.c_int
         lib.aqlm_status_string.argtypes = [ctypes.c_int]
         lib.aqlm_status_string.restype = ctypes.c_char_p
         _lib = lib

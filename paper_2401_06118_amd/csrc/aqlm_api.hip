@@ -265,6 +265,21 @@ int aqlm_backward(const void* codes, const uint16_t* codebooks, const uint16_t* 
   return status_of(aqlm::launch_backward(L, (int32_t)n, x, dy, dcodebooks, dscales, static_cast<hipStream_t>(stream)));
 }
 
+int aqlm_beam_search(const float* w, const float* h, void* codes, const uint16_t* codebooks, const uint16_t* scales,
+                     int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int32_t beam, int32_t sweeps,
+                     float* loss_out, void* stream) {
+  aqlm::Layer L;
+  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  if (!w || !h) return AQLM_ERR_NULL;
+  if (beam < 1 || sweeps < 0 || d_in >= (int64_t(1) << 16)) return AQLM_ERR_SHAPE;
+  if (B != 8 || !aqlm::beam_search_fits((int32_t)d_in, M, beam)) return AQLM_ERR_UNSUPPORTED;
+  if (!aligned(w, 4) || !aligned(h, 4) || (loss_out && !aligned(loss_out, 4))) return AQLM_ERR_ALIGN;
+  return status_of(aqlm::launch_beam_search(w, h, static_cast<uint8_t*>(const_cast<void*>(codes)), codebooks, scales,
+                                            (int32_t)d_out, (int32_t)d_in, M, beam, sweeps, loss_out,
+                                            static_cast<hipStream_t>(stream)));
+}
+
 int aqlm_gemm_noalloc(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                       int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
                       void* stream) {

@@ -83,6 +83,13 @@ bool backward_supported(const Layer& L);
 hipError_t launch_backward(const Layer& L, int32_t n, const uint16_t* x, const uint16_t* dy, float* dcb, float* ds,
                            hipStream_t s);
 
+// Phase-1 beam search over codes (8-bit codes), one workgroup per row, the
+// beam state in LDS.
+bool beam_search_fits(int32_t d_in, int32_t M, int32_t beam);
+hipError_t launch_beam_search(const float* w, const float* h, uint8_t* codes, const uint16_t* codebooks,
+                              const uint16_t* scales, int32_t d_out, int32_t d_in, int32_t M, int32_t beam,
+                              int32_t sweeps, float* loss, hipStream_t s);
+
 int num_cus();
 // Allows a kernel `bytes` of dynamic LDS on the current device (once per
 // kernel, device and size).

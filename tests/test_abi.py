@@ -205,3 +205,16 @@ def test_backward_refuses_before_launch(lib):
     assert call(M=2, B=12) == UNSUP
     assert call(dy=P + 2) == ALIGN
     assert call(ds=P + 2) == ALIGN
+
+
+def test_beam_search_refuses_before_launch(lib):
+    def call(w=P, h=P, codes=P, d_out=8, d_in=64, M=2, B=8, beam=4, sweeps=1, loss=P):
+        return lib.aqlm_beam_search(w, h, codes, P, P, d_out, d_in, M, B, 8, beam, sweeps, loss, None)
+    assert call(w=None) == NULL
+    assert call(h=None) == NULL
+    assert call(beam=0) == SHAPE
+    assert call(sweeps=-1) == SHAPE
+    assert call(M=1, B=16) == UNSUP
+    assert call(beam=9) == UNSUP
+    assert call(d_in=4096, beam=8) == UNSUP      # state beyond the on-chip budget
+    assert call(w=P + 2) == ALIGN

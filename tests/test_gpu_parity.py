@@ -729,6 +729,64 @@ def test_backward_refuses_before_launch():
         aq().backward(c16, cb16, sc16, x16, dy)
 
 
+# ----------------------------------------------------- Phase 1: beam search
+
+BEAM_CASES = [
+    # (d_out, d_in, M, beam, sweeps)
+    (16, 64, 2, 4, 2),
+    (32, 128, 1, 1, 1),
+    (24, 256, 3, 8, 1),
+    (8, 512, 2, 2, 1),
+    (40, 1024, 2, 4, 1),
+    (6, 2048, 1, 8, 1),     # the largest state for beam 8
+]
+
+
+def _beam_inputs(seed, d_out, d_in, M, n_x=64):
+    rng = np.random.default_rng(seed)
+    lay = synth.layer(seed, d_out, d_in, M, 8)
+    x = rng.integers(-3, 4, size=(d_in, n_x)).astype(np.float32)  # X X^T exact in fp32
+    h = (x.astype(np.float64) @ x.T.astype(np.float64)).astype(np.float32)
+    w = (rng.standard_normal((d_out, d_in)) * 0.05).astype(np.float32)
+    return lay, w, h
+
+
+@pytest.mark.parametrize("d_out,d_in,M,beam,sweeps", BEAM_CASES)
+def test_beam_search_matches_oracle(d_out, d_in, M, beam, sweeps):
+    """The GPU search scores candidates with fp32 increments, the oracle in
+    fp64, so a near-tie can go either way and the paths may then part: most
+    rows must end on exactly the oracle's codes, every row within 2e-3 of the
+    oracle's loss, never above its starting loss, and the reported loss must
+    be the exact loss of the returned codes."""
+    print(f"[beam] d_out={d_out} d_in={d_in} M={M} beam={beam} sweeps={sweeps}", flush=True)
+    lay, w, h = _beam_inputs(30000 + d_in + M + beam, d_out, d_in, M)
+    ref_codes, ref_loss = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=beam, sweeps=sweeps)
+    codes, cb, sc, _ = to_device(lay)
+    loss = aq().beam_search(torch.from_numpy(w).cuda(), torch.from_numpy(h).cuda(), codes, cb, sc, beam=beam,
+                            sweeps=sweeps)
+    torch.cuda.synchronize()
+    got = codes.cpu().numpy()
+    got_loss = loss.double().cpu().numpy()
+    exact = oracle.aq_loss(w, h, got, lay.codebooks, lay.scales)
+    np.testing.assert_allclose(got_loss, exact, rtol=1e-6)
+    np.testing.assert_allclose(exact, ref_loss, rtol=2e-3)
+    differ = np.flatnonzero((got != ref_codes).any(axis=(1, 2)))
+    print(f"[beam] rows with other codes than the oracle: {differ.size} of {d_out}", flush=True)
+    assert differ.size <= max(1, d_out // 4), differ
+    start = oracle.aq_loss(w, h, lay.codes, lay.codebooks, lay.scales)
+    assert np.all(exact <= start * (1 + 1e-6))
+
+
+def test_beam_search_refuses_before_launch():
+    lay, w, h = _beam_inputs(30100, 8, 4096, 2)
+    codes, cb, sc, _ = to_device(lay)
+    before = codes.clone()
+    with pytest.raises(aq().AqlmError):          # beam 8 x 4096 inputs: state beyond the on-chip budget
+        aq().beam_search(torch.from_numpy(w).cuda(), torch.from_numpy(h).cuda(), codes, cb, sc, beam=8)
+    torch.cuda.synchronize()
+    assert torch.equal(codes, before)
+
+
 # -------------------------------------------------- 1x15 (15-bit codes)
 
 @pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (11008, 4096), (4096, 11008), (1000, 4104), (37, 8)])
