@@ -351,10 +351,20 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
 #pragma unroll
   for (int i = 0; i < kAhead; ++i) issue_rb(i / RB, i % RB, ring[i / RB][i % RB]);
 
-  // 3. stage codebook copies and x.
+  // 3. stage codebook copies and x.  Eight copies of two codebooks (x too
+  // large for sixteen) are interleaved per codeword: entry e holds the 8
+  // copies of codebook 0, then the 8 of codebook 1 (256 bytes, every 16-byte
+  // bank group once).  Lanes 8-15 of each 16-lane group then gather the
+  // other code of the group (same x, other codebook) in the same
+  // instruction, so the 16 lanes of one LDS pass read 16 different bank
+  // groups; each row still gets both codebooks over the pair of MFMAs.
+  constexpr bool kPairCb = COPIES == 8 && M == 2;
   if (tid < M * 256) {
 #pragma unroll
-    for (int k = 0; k < COPIES; ++k) cb_lds[tid * COPIES + ((k + lane) % COPIES)] = cbv;
+    for (int k = 0; k < COPIES; ++k) {
+      const int c = (k + lane) % COPIES;
+      cb_lds[kPairCb ? (tid & 255) * 16 + (tid >> 8) * 8 + c : tid * COPIES + c] = cbv;
+    }
   }
 #pragma unroll
   for (int i = 0; i < C::kXL; ++i) {
@@ -369,6 +379,18 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   uint32_t base_m[M];
 #pragma unroll
   for (int m = 0; m < M; ++m) base_m[m] = cb_base + ((uint32_t)m << 16) + copy_off;
+  // interleaved layout: address (code * 16 + m * 8 + copy) * 16, with m and
+  // the code byte (t ^ flip) flipped on lanes 8-15
+  const uint32_t flip = (uint32_t)(r16 >> 3);
+  uint32_t pbase[2], psel[4];
+#pragma unroll
+  for (int tm = 0; tm < 2; ++tm) pbase[tm] = cb_base + ((((uint32_t)tm ^ flip) * 8u + (uint32_t)(lane % 8)) * 16u);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) psel[k] = 0x0C020000u | ((4u + ((uint32_t)k ^ flip)) << 8);
+  auto gaddr = [&](uint32_t word, int t) -> uint32_t {
+    if constexpr (kPairCb) return __builtin_amdgcn_perm(word, pbase[t % 2], psel[t % 4]);
+    return cw_addr<M, COPIES>(word, t % 4, base_m[t % M], copy_off + cb_base, t % M);
+  };
   {
     f4_t acc[RB];
 #pragma unroll
@@ -413,11 +435,8 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
 #pragma unroll
               for (int u = 0; u < kStep; ++u) {
                 const int t = t0 + u;
-                av[u] = lds_load16(
-                    cw_addr<M, COPIES>(ring[d][rb][t / 4], t % 4, base_m[t % M], copy_off + cb_base, t % M));
-                if (pair)
-                  bv[u] = lds_load16(cw_addr<M, COPIES>(ring[d][pair ? rb + 1 : rb][t / 4], t % 4, base_m[t % M],
-                                                        copy_off + cb_base, t % M));
+                av[u] = lds_load16(gaddr(ring[d][rb][t / 4], t));
+                if (pair) bv[u] = lds_load16(gaddr(ring[d][pair ? rb + 1 : rb][t / 4], t));
               }
               // All the step's gathers go out before its first MFMA.  Left
               // alone, the scheduler pairs each gather with its MFMA, so every

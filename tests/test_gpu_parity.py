@@ -159,6 +159,19 @@ def test_gemv_1x16_codebook_chunks(shapes):
         _grouped_case(shapes, 1, 16, 9200)
 
 
+@pytest.mark.parametrize("shapes", [[(300, 20480)], [(1000, 16384)], [(77, 28672)], [(512, 16384), (96, 20480)]])
+def test_gemv_eight_codebook_copies(shapes):
+    """2x8 layers wide enough that x leaves room for only 8 codebook copies:
+    the interleaved copy layout where lanes 8-15 gather the other codebook."""
+    print(f"[gemv-8copies] {shapes}", flush=True)
+    if len(shapes) == 1:
+        lay = synth.layer(3100 + shapes[0][1], shapes[0][0], shapes[0][1], 2, 8)
+        codes, cb, sc, x = to_device(lay)
+        check_products(lay, fp16_to_np(aq().gemv(codes, cb, sc, x[0]))[None, :])
+    else:
+        _grouped_case(shapes, 2, 8, 3200)
+
+
 def test_gemv_70b_shapes_sampled_rows():
     """Llama-2-70B-shaped 2x8 layers: gate/up 28672 x 8192, down 8192 x 28672,
     k/v 1024 x 8192; outputs checked on sampled rows."""
