@@ -59,6 +59,10 @@ def _load():
     lib.oracle_aq_loss.restype = ctypes.c_int
     lib.oracle_beam_search.argtypes = [p, p, p, p, p, i64, i64, i32, i32, i32, i32, i32, p]
     lib.oracle_beam_search.restype = ctypes.c_int
+    lib.oracle_packed_row_bytes.argtypes = [i64, i32, i32, i32]
+    lib.oracle_packed_row_bytes.restype = ctypes.c_int64
+    lib.oracle_unpack_codes.argtypes = [p, i64, i64, i32, i32, i32, p]
+    lib.oracle_unpack_codes.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_threads.argtypes = [ctypes.c_int]
@@ -219,3 +223,26 @@ def beam_search(w, h, codes, codebooks, scales, beam: int, sweeps: int = 1, g: i
     _check(_load().oracle_beam_search(_ptr(wf), _ptr(hf), _ptr(out), _ptr(cb), _ptr(sc), d_out, d_in, M, B, g,
                                       int(beam), int(sweeps), _ptr(loss)))
     return out, loss
+
+
+def unpack_codes(packed, d_out: int, d_in: int, M: int, B: int, g: int = 8) -> np.ndarray:
+    """Codes [d_out, d_in/g, M] (uint16) from bit-packed rows (see aqlm_oracle.c)."""
+    lib = _load()
+    pitch = int(lib.oracle_packed_row_bytes(d_in, M, B, g))
+    pk = np.ascontiguousarray(np.asarray(packed, dtype=np.uint8)).reshape(-1)
+    if pk.size != d_out * pitch:
+        raise ValueError(f"packed codes must hold {d_out} rows of {pitch} bytes")
+    out = np.empty((d_out, d_in // g, M), dtype=np.uint16)
+    _check(lib.oracle_unpack_codes(_ptr(pk), d_out, d_in, M, B, g, _ptr(out)))
+    return out
+
+
+def dequantize_packed(packed, codebooks, scales, d_in: int, B: int, g: int = 8) -> np.ndarray:
+    """Dequantized weights (fp16 bits) of a layer with bit-packed B-bit codes."""
+    cb = _bits16(codebooks)
+    M = cb.shape[0]
+    d_out = np.asarray(scales).shape[0]
+    codes = unpack_codes(packed, d_out, d_in, M, B, g)
+    if (1 << B) != cb.shape[1]:
+        raise ValueError("codebooks must hold 2^B codewords")
+    return dequantize(codes if B > 8 else codes.astype(np.uint8), codebooks, scales, g)

@@ -120,6 +120,36 @@ void oracle_f16_to_f32_array(const uint16_t* in, float* out, int64_t n) {
   for (int64_t i = 0; i < n; ++i) out[i] = oracle_f16_to_f32(in[i]);
 }
 
+/* ---- bit-packed codes ----
+ * A row of packed B-bit codes is its codes in index order q = j*M + m as one
+ * little-endian bit string: code q is bits [q*B, (q+1)*B) of the row, bit b
+ * being bit b % 8 of byte b / 8; the row is padded with zero bits to a whole
+ * number of 32-bit words, so a row takes ceil(G*M*B / 32) * 4 bytes. */
+int64_t oracle_packed_row_bytes(int64_t d_in, int32_t M, int32_t B, int32_t g) {
+  const int64_t bits = (d_in / g) * M * B;
+  return (bits + 31) / 32 * 4;
+}
+
+/* Unpack [d_out] packed rows into codes [d_out][G][M] (uint16). */
+int oracle_unpack_codes(const uint8_t* packed, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                        uint16_t* codes) {
+  if (!packed || !codes) return ORC_ERR_NULL;
+  if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return ORC_ERR_SHAPE;
+  if (B < 1 || B > 16 || M < 1) return ORC_ERR_UNSUPPORTED;
+  const int64_t n = (d_in / g) * M;
+  const int64_t pitch = oracle_packed_row_bytes(d_in, M, B, g);
+  for (int64_t i = 0; i < d_out; ++i)
+    for (int64_t q = 0; q < n; ++q) {
+      uint32_t v = 0;
+      for (int32_t b = 0; b < B; ++b) {
+        const int64_t bit = q * B + b;
+        v |= (uint32_t)((packed[i * pitch + bit / 8] >> (bit % 8)) & 1u) << b;
+      }
+      codes[i * n + q] = (uint16_t)v;
+    }
+  return ORC_OK;
+}
+
 /* ---- dequantization (Eq. 2 with per-output scales, Fig. 3 steps i-v) ---- */
 
 static int check_args(const void* codes, const uint16_t* codebooks, const uint16_t* scales,

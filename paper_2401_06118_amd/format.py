@@ -77,3 +77,26 @@ def model_bits_per_param(model: str, M: int, B: int, g: int = 8) -> float:
     bits = sum(AqlmShape(o, i, M, B, g).storage_bits() for o, i in projs) * n_layers
     params = sum(o * i for o, i in projs) * n_layers
     return bits / params
+
+
+def packed_row_bytes(d_in: int, M: int, B: int, g: int = 8) -> int:
+    """Bytes of one row of bit-packed codes: G*M codes of B bits, padded to
+    whole 32-bit words (the library's packed layout)."""
+    return ((d_in // g) * M * B + 31) // 32 * 4
+
+
+def pack_codes(codes, B: int):
+    """Bit-pack codes [d_out, G, M] (values < 2^B): each row's codes in index
+    order j*M + m as a little-endian bit string (code q at bits [q*B, (q+1)*B)),
+    zero-padded to whole 32-bit words; returns uint8 [d_out, row bytes]."""
+    import numpy as np
+    c = np.asarray(codes).astype(np.uint64)
+    d_out, G, M = c.shape
+    n = G * M
+    flat = c.reshape(d_out, n)
+    pitch = packed_row_bytes(G * 8, M, B)
+    bits = ((flat[:, :, None] >> np.arange(B, dtype=np.uint64)[None, None, :]) & 1).astype(np.uint8)
+    bits = bits.reshape(d_out, n * B)
+    pad = pitch * 8 - n * B
+    bits = np.concatenate([bits, np.zeros((d_out, pad), np.uint8)], axis=1)
+    return np.packbits(bits.reshape(d_out, pitch, 8), axis=2, bitorder="little").reshape(d_out, pitch)

@@ -523,3 +523,30 @@ def test_beam_search_more_sweeps_never_worse():
     _, l1 = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=3, sweeps=1)
     _, l3 = oracle.beam_search(w, h, lay.codes, lay.codebooks, lay.scales, beam=3, sweeps=3)
     assert np.all(l3 <= l1 * (1 + 1e-12))
+
+
+# ------------------------------------------------------------ bit-packed codes
+
+@pytest.mark.parametrize("M,B,d_in", [(1, 15, 64), (2, 12, 40), (2, 15, 24), (1, 16, 16), (3, 5, 8), (2, 8, 64)])
+def test_packed_codes_round_trip_and_bit_positions(M, B, d_in):
+    """The oracle's unpacking inverts the packer (two independent
+    implementations of the layout), a row takes ceil(G*M*B/32)*4 bytes, and
+    code q sits at bits [q*B, (q+1)*B) (checked bit by bit on one row)."""
+    rng = np.random.default_rng(80 + M + B)
+    d_out = 5
+    codes = rng.integers(0, 1 << B, size=(d_out, d_in // 8, M)).astype(np.uint16)
+    packed = fmt.pack_codes(codes, B)
+    assert packed.shape == (d_out, ((d_in // 8) * M * B + 31) // 32 * 4)
+    assert np.array_equal(oracle.unpack_codes(packed, d_out, d_in, M, B), codes)
+    bitstr = "".join(f"{b:08b}"[::-1] for b in packed[2])
+    flat = codes[2].reshape(-1)
+    for q, v in enumerate(flat):
+        assert int(bitstr[q * B:(q + 1) * B][::-1], 2) == int(v)
+    assert set(bitstr[len(flat) * B:]) <= {"0"}
+
+
+def test_packed_dequantize_matches_unpacked():
+    lay = synth.layer(85, 33, 96, 2, 12)
+    packed = fmt.pack_codes(lay.codes, 12)
+    assert np.array_equal(oracle.dequantize_packed(packed, lay.codebooks, lay.scales, 96, 12),
+                          oracle.dequantize(lay.codes, lay.codebooks, lay.scales))
