@@ -85,6 +85,8 @@ def parse_args():
                          "through both kernel families (codeword gathers, partial-product tables) and exit")
     ap.add_argument("--backward", action="store_true",
                     help="only time the gradients through Eq. 2 (aqlm_backward) and exit")
+    ap.add_argument("--single-layers", action="store_true",
+                    help="only the single-layer matrix-vector rows (incl. bit-packed codes)")
     ap.add_argument("--beam-search", action="store_true",
                     help="only time the Phase-1 beam search (aqlm_beam_search) and exit")
     ap.add_argument("--once", action="store_true",
@@ -96,11 +98,12 @@ def parse_args():
 
 
 class DeviceLayer:
-    def __init__(self, seed, d_out, d_in, M, B, n=1, x=None):
+    def __init__(self, seed, d_out, d_in, M, B, n=1, x=None, packed=False):
         from paper_2401_06118_amd import format as fmt
         from paper_2401_06118_amd import synth
         self.shape = fmt.AqlmShape(d_out, d_in, M, B)
-        self.codes, self.codebooks, self.scales, xg = synth.device_layer(seed, d_out, d_in, M, B, n=n)
+        make = synth.device_packed_layer if packed else synth.device_layer
+        self.codes, self.codebooks, self.scales, xg = make(seed, d_out, d_in, M, B, n=n)
         self.x = xg if x is None else x
         import torch
         self.y = torch.empty((n, d_out), dtype=torch.float16, device="cuda")
@@ -392,18 +395,26 @@ def single_layer_rows(aq, torch):
         "11008x4096 2x12": (11008, 4096, 2, 12),
         "11008x4096 2x16": (11008, 4096, 2, 16),
         "28672x8192 2x8": (28672, 8192, 2, 8),
+        "11008x4096 2x15": (11008, 4096, 2, 15),
+        # bit-packed codes (B bits per code, rows padded to 32-bit words)
+        "11008x4096 2x12 packed": (11008, 4096, 2, 12),
+        "11008x4096 2x15 packed": (11008, 4096, 2, 15),
+        "11008x4096 1x15 packed": (11008, 4096, 1, 15),
+        "4096x4096 2x12 packed": (4096, 4096, 2, 12),
     }.items():
         from paper_2401_06118_amd import format as fmt
+        packed = name.endswith("packed")
         shp = fmt.AqlmShape(d_out, d_in, M, B)
-        reps = max(2, min(256, (1 << 30) // shp.codes_bytes() + 1))
-        layers = [DeviceLayer(900000 + i, d_out, d_in, M, B) for i in range(reps)]
+        code_bytes = shp.packed_codes_bytes() if packed else shp.codes_bytes()
+        reps = max(2, min(256, (1 << 30) // code_bytes + 1))
+        layers = [DeviceLayer(900000 + i, d_out, d_in, M, B, packed=packed) for i in range(reps)]
         calls = [lambda L=L: L.gemv(aq) for L in layers]
         g = graph_of(calls)
         ms = time_steps(g.replay, steps=3, warmup=1) / reps
         pair = per_launch_ms(calls[: min(reps, 64)], reps=2)
         pair_ms = sum(pair) / len(pair)
         del g
-        b = shp.gemv_bytes(1)
+        b = shp.packed_gemv_bytes(1) if packed else shp.gemv_bytes(1)
         rows.append({"layer": name, "bytes": b, "us_per_call": ms * 1e3, "frac_per_call": b / (ms * 1e6) / HBM_PEAK_GBS,
                      "GBs_per_call": b / (ms * 1e6), "event_pair_us": pair_ms * 1e3,
                      "GBs_event_pair": b / (pair_ms * 1e6), "replicas": reps})
@@ -624,6 +635,9 @@ def main():
         return
     if args.beam_search:
         print(json.dumps({"beam_search": beam_rows(aq, torch)}), flush=True)
+        return
+    if args.single_layers:
+        print(json.dumps({"single_layers": single_layer_rows(aq, torch)}), flush=True)
         return
     if args.compare_paths:
         print(json.dumps({"paths": compare_paths(aq, torch, once=args.once)}), flush=True)

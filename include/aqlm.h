@@ -34,7 +34,17 @@
  *   B = 15 or 16, M = 1   one codebook of 32768 or 65536 entries (2 bits);
  *   B = 12, M = 2         two codebooks of 4096 entries (3 bits);
  *   B = 15 or 16, M = 2   two codebooks of 32768 or 65536 entries (4 bits).
- * Codes wider than 8 bits are stored one per uint16, without bit packing.
+ * Codes wider than 8 bits are stored one per uint16 by default.  Bit-packed
+ * codes (the storage the paper's bits-per-parameter figures count, Sec. 3.3):
+ * pass B | AQLM_PACKED for B = 12 (M = 2) or 15 (M = 1 or 2).  Each row of
+ * codes is then one bit string of d_in/g * M codes of B bits, code (j, m)
+ * at bits [(j*M + m)*B, (j*M + m + 1)*B), least significant bit first,
+ * zero-padded to whole little-endian 32-bit words: aqlm_packed_row_words()
+ * words per row, rows contiguous.  Only aqlm_dequantize, aqlm_gemv and
+ * aqlm_gemv_grouped (gather path) accept packed codes; every other entry
+ * point returns AQLM_ERR_UNSUPPORTED for them, as does aqlm_gemv when x
+ * does not fit the matrix-core kernel's staging (d_in above 65536).  A
+ * packed row must hold fewer than 2^32 bits (else AQLM_ERR_SHAPE).
  * Sizes: d_out * (d_in / g) must stay below 2^31 and d_out, d_in, n below
  * 2^31.
  *
@@ -70,6 +80,13 @@ enum aqlm_status {
   AQLM_ERR_WORKSPACE = 6,   /* aqlm_gemm: workspace smaller than aqlm_gemm_workspace_bytes */
   AQLM_ERR_SCRATCH = 7      /* aqlm_gemm_noalloc: the product needs more than its fixed scratch */
 };
+
+/* OR into B to pass bit-packed codes (see "Bit-packed codes" above). */
+#define AQLM_PACKED 0x100
+
+/* 32-bit words that hold one row of bit-packed codes: ceil(d_in/g * M * B / 32)
+ * (B without AQLM_PACKED).  Host function; returns 0 for a non-positive size. */
+int64_t aqlm_packed_row_words(int64_t d_in, int32_t M, int32_t B, int32_t g);
 
 /* Dequantize: w_out[i][j*g + k] = fp16(fp32(sum_m C_m[b[i][j][m]][k]) * s_i)
  * (Eq. 2, Fig. 3 steps i-v).  The M codewords are added in fp32 in ascending m,

@@ -18,8 +18,12 @@ Every computation runs in the hand-written HIP kernels of
 ``libaqlm_mi355x.so``; this module only marshals arguments.
 
 Tensor formats: ``codes`` uint8 [d_out, d_in/8, M] (B = 8) or uint16/int16
-[d_out, d_in/8, 1] (B = 16); ``codebooks`` fp16 [M, 2^B, 8]; ``scales`` fp16
-[d_out] (a trailing singleton dimension is accepted); activations fp16.
+[d_out, d_in/8, M] (B = 12, 15, 16); ``codebooks`` fp16 [M, 2^B, 8]; ``scales``
+fp16 [d_out] (a trailing singleton dimension is accepted); activations fp16.
+:func:`dequantize`, :func:`gemv` and :func:`gemv_grouped` also take bit-packed
+codes (B = 12 or 15): int32 [d_out, row words], each row a little-endian bit
+string of its d_in/8 * M codes (code (j, m) at bits (j*M + m)*B ..), zero-padded
+to whole 32-bit words (``format.pack_codes`` writes it).
 """
 from __future__ import annotations
 
@@ -31,7 +35,7 @@ from ._lib import AqlmError, status_string  # noqa: F401
 __all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "gemm_workspace_bytes", "gemm", "backward",
            "beam_search",
            "AqlmError",
-           "status_string", "layer_args"]
+           "status_string", "layer_args", "packed_layer_args"]
 
 
 def _stream_handle(stream) -> int:
@@ -64,6 +68,42 @@ def layer_args(codes: torch.Tensor, codebooks: torch.Tensor, scales: torch.Tenso
     return d_out, groups * g, M, B, g
 
 
+def packed_layer_args(words: torch.Tensor, codebooks: torch.Tensor, scales: torch.Tensor, d_in: int):
+    """Validate bit-packed codes (int32 [d_out, row words]) and return
+    (d_out, d_in, M, B | PACKED, g) for the C ABI."""
+    for name, t in (("codes", words), ("codebooks", codebooks), ("scales", scales)):
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if codebooks.dtype != torch.float16 or codebooks.dim() != 3:
+        raise ValueError("codebooks must be fp16 [M, 2^B, g]")
+    M, entries, g = codebooks.shape
+    B = int(entries).bit_length() - 1
+    if (1 << B) != entries:
+        raise ValueError("codebook entry count must be a power of two")
+    if words.dtype != torch.int32 or words.dim() != 2:
+        raise ValueError("packed codes must be int32 [d_out, row words]")
+    d_in = int(d_in)
+    if d_in <= 0 or d_in % g != 0:
+        raise ValueError(f"d_in must be a positive multiple of {g}")
+    row_words = ((d_in // g) * M * B + 31) // 32
+    if words.shape[1] != row_words:
+        raise ValueError(f"packed codes of d_in={d_in}, M={M}, B={B} have {row_words} words per row")
+    if scales.dtype != torch.float16 or scales.numel() != words.shape[0]:
+        raise ValueError("scales must be fp16 with one value per output row")
+    return words.shape[0], d_in, M, B | _lib.PACKED, g
+
+
+def _args(codes, codebooks, scales, d_in):
+    """layer_args, or packed_layer_args for 2-D (bit-packed) codes."""
+    if codes.dim() == 2:
+        if d_in is None:
+            raise ValueError("bit-packed codes need d_in")
+        return packed_layer_args(codes, codebooks, scales, d_in)
+    return layer_args(codes, codebooks, scales)
+
+
 def _out(out, shape, like: torch.Tensor) -> torch.Tensor:
     """A caller's output tensor, checked like the inputs (the C ABI cannot see
     sizes, so an undersized buffer would be written past its end), or a new
@@ -86,9 +126,10 @@ def _check(st: int, what: str):
         raise AqlmError(st, what)
 
 
-def dequantize(codes, codebooks, scales, *, out=None, stream=None) -> torch.Tensor:
-    """fp16 weight matrix [d_out, d_in]: w[i, 8j+k] = fp16(sum_m C_m[b_ijm][k] * s_i)."""
-    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+def dequantize(codes, codebooks, scales, *, d_in=None, out=None, stream=None) -> torch.Tensor:
+    """fp16 weight matrix [d_out, d_in]: w[i, 8j+k] = fp16(sum_m C_m[b_ijm][k] * s_i).
+    ``d_in`` is needed (only) for bit-packed codes."""
+    d_out, d_in, M, B, g = _args(codes, codebooks, scales, d_in)
     out = _out(out, (d_out, d_in), codes)
     st = _lib.load().aqlm_dequantize(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(), d_out, d_in,
                                      M, B, g, out.data_ptr(), _stream_handle(stream))
@@ -98,7 +139,7 @@ def dequantize(codes, codebooks, scales, *, out=None, stream=None) -> torch.Tens
 
 def gemv(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:
     """y [d_out] = W x for one fp16 activation vector x [d_in]."""
-    d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+    d_out, d_in, M, B, g = _args(codes, codebooks, scales, x.numel())
     if x.dtype != torch.float16 or x.numel() != d_in or not x.is_cuda or not x.is_contiguous():
         raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
     out = _out(out, (d_out,), codes)
@@ -121,7 +162,7 @@ def gemv_grouped(problems, *, path: str = "auto", stream=None):
     arr = (_lib.GemvProblem * len(problems))()
     fmt = None
     for i, (codes, codebooks, scales, x, y) in enumerate(problems):
-        d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+        d_out, d_in, M, B, g = _args(codes, codebooks, scales, x.numel())
         if fmt is None:
             fmt = (M, B, g)
         elif fmt != (M, B, g):

@@ -20,8 +20,9 @@ STATUS_NAMES = {0: "AQLM_OK", 1: "AQLM_ERR_NULL", 2: "AQLM_ERR_SHAPE", 3: "AQLM_
 PATH_AUTO, PATH_GATHER, PATH_TABLE = 0, 1, 2
 EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemv_grouped_path", "aqlm_gemm_small_batch",
            "aqlm_gemm_workspace_bytes", "aqlm_gemm", "aqlm_gemm_noalloc", "aqlm_backward", "aqlm_beam_search",
-           "aqlm_status_string")
+           "aqlm_packed_row_words", "aqlm_status_string")
 MAX_GROUPED = 8
+PACKED = 0x100  # OR-ed into B: bit-packed codes
 
 
 class GemvProblem(ctypes.Structure):
@@ -74,6 +75,8 @@ def load():
         lib.aqlm_backward.restype = ctypes.c_int
         lib.aqlm_beam_search.argtypes = [p, p, p, p, p, i64, i64, i32, i32, i32, i32, i32, p, p]
         lib.aqlm_beam_search.restype = ctypes.c_int
+        lib.aqlm_packed_row_words.argtypes = [i64, i32, i32, i32]
+        lib.aqlm_packed_row_words.restype = ctypes.c_int64
         lib.aqlm_status_string.argtypes = [ctypes.c_int]
         lib.aqlm_status_string.restype = ctypes.c_char_p
         _lib = lib

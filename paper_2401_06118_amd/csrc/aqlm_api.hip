@@ -81,16 +81,22 @@ void* scratch_ptr() {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
+// allow_packed: the entry point takes bit-packed codes (B | AQLM_PACKED).
 int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
-                int32_t M, int32_t B, int32_t g, aqlm::Layer* L) {
+                int32_t M, int32_t B, int32_t g, aqlm::Layer* L, bool allow_packed = false) {
   if (!codes || !codebooks || !scales) return AQLM_ERR_NULL;
   if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return AQLM_ERR_SHAPE;
   if (g != 8) return AQLM_ERR_UNSUPPORTED;
+  const bool packed = (B & AQLM_PACKED) != 0;
+  B &= ~AQLM_PACKED;
+  if (packed && (!allow_packed || !aqlm::packed_supported(M, B))) return AQLM_ERR_UNSUPPORTED;
   if (!aqlm::format_supported(M, B)) return AQLM_ERR_UNSUPPORTED;
   const int64_t G = d_in / g;
   // (sizes and offsets are held in 32 bits on the device side)
   if (d_out >= (int64_t(1) << 31) || d_in >= (int64_t(1) << 31) || d_out * G >= (int64_t(1) << 31))
     return AQLM_ERR_SHAPE;
+  // (bit offsets within a packed row are held in 32 bits)
+  if (packed && G * M * B >= (int64_t(1) << 32)) return AQLM_ERR_SHAPE;
   if (!aligned(codes, 16) || !aligned(codebooks, 16) || !aligned(scales, 2)) return AQLM_ERR_ALIGN;
   L->codes = codes;
   L->codebooks = codebooks;
@@ -101,7 +107,8 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
   L->M = M;
   L->B = B;
   const int64_t pitch = G * M * (B > 8 ? 2 : 1);
-  L->vec_codes = (pitch % 16) == 0;
+  L->packed = packed;
+  L->vec_codes = packed || (pitch % 16) == 0;  // (packed rows are read as 32-bit words)
   return AQLM_OK;
 }
 
@@ -156,7 +163,7 @@ extern "C" {
 int aqlm_dequantize(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                     int64_t d_in, int32_t M, int32_t B, int32_t g, uint16_t* w_out, void* stream) {
   aqlm::Layer L;
-  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L, true);
   if (st != AQLM_OK) return st;
   if (!w_out) return AQLM_ERR_NULL;
   if (!aligned(w_out, 16)) return AQLM_ERR_ALIGN;
@@ -166,10 +173,11 @@ int aqlm_dequantize(const void* codes, const uint16_t* codebooks, const uint16_t
 int aqlm_gemv(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
               int32_t M, int32_t B, int32_t g, const uint16_t* x, uint16_t* y, void* stream) {
   aqlm::Layer L;
-  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L, true);
   if (st != AQLM_OK) return st;
   if (!x || !y) return AQLM_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
+  if (L.packed && !aqlm::gemv_mfma_fits(&L, 1)) return AQLM_ERR_UNSUPPORTED;
   return status_of(gemv_dispatch(L, x, y, static_cast<hipStream_t>(stream)));
 }
 
@@ -316,7 +324,7 @@ int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int
   uint16_t* ys[AQLM_MAX_GROUPED];
   for (int i = 0; i < count; ++i) {
     const aqlm_gemv_problem& P = problems[i];
-    const int st = check_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &Ls[i]);
+    const int st = check_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &Ls[i], true);
     if (st != AQLM_OK) return st;
     if (!P.x || !P.y) return AQLM_ERR_NULL;
     if (!aligned(P.x, 16) || !aligned(P.y, 16)) return AQLM_ERR_ALIGN;
@@ -324,6 +332,11 @@ int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int
     ys[i] = P.y;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (Ls[0].packed) {
+    // packed codes: the gather kernel only, all problems in one launch
+    if (path == AQLM_PATH_TABLE || !aqlm::gemv_mfma_fits(Ls, count)) return AQLM_ERR_UNSUPPORTED;
+    return status_of(aqlm::launch_gemv_mfma(Ls, xs, ys, count, s));
+  }
   if (path == AQLM_PATH_TABLE) {
     if (!aqlm::gemv_lut_supported(Ls, count)) return AQLM_ERR_UNSUPPORTED;
     return status_of(aqlm::launch_gemv_lut(Ls, xs, ys, count, s));
@@ -337,6 +350,11 @@ int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int
     if (e != hipSuccess) return AQLM_ERR_HIP;
   }
   return AQLM_OK;
+}
+
+int64_t aqlm_packed_row_words(int64_t d_in, int32_t M, int32_t B, int32_t g) {
+  if (d_in <= 0 || M <= 0 || B <= 0 || g <= 0) return 0;
+  return ((d_in / g) * M * (int64_t)(B & ~AQLM_PACKED) + 31) / 32;
 }
 
 const char* aqlm_status_string(int status) {

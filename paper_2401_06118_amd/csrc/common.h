@@ -9,6 +9,10 @@ typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
 typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+// 3 and 4 words at a dword-aligned address (global loads of several dwords
+// need only dword alignment)
+typedef uint32_t u32x3a4_t __attribute__((ext_vector_type(3), aligned(4)));
+typedef uint32_t u32x4a4_t __attribute__((ext_vector_type(4), aligned(4)));
 
 namespace aqlm {
 

@@ -4,7 +4,8 @@
 //   w   = fp16_rne(acc * s_i)                                     (one fp32 product)
 // Each thread writes one group of 8 weights (16 bytes); consecutive threads
 // write consecutive groups, so both the code reads and the fp16 writes are
-// fully coalesced.  The kernel is bound by the 16-byte-per-group write
+// fully coalesced.  Bit-packed codes (12 or 15 bits) are cut out of the
+// one or two 32-bit words that hold the group.  The kernel is bound by the 16-byte-per-group write
 // stream.  For B = 8 the M codebooks (4 KiB each) sit in LDS; wider codes
 // read their codebooks (up to 2 x 1 MiB) through L2.
 #include "common.h"
@@ -47,6 +48,20 @@ __device__ __forceinline__ void load_group_codes(const void* __restrict__ codes,
   }
 }
 
+// Codes of group j of a row of bit-packed codes (words: the row's 32-bit
+// words): code m is bits [(j*M + m)*B, + B) of the row, at most two words.
+template <int M, int B>
+__device__ __forceinline__ void load_group_codes_packed(const uint32_t* __restrict__ words, uint32_t j,
+                                                        uint32_t (&c)[M]) {
+  const uint32_t bit = j * (uint32_t)(M * B);
+  const uint32_t w0 = bit >> 5, sh = bit & 31u;
+  uint64_t v = words[w0];
+  if (sh + (uint32_t)(M * B) > 32u) v |= (uint64_t)words[w0 + 1] << 32;  // (inside the row: the codes end there)
+  v >>= sh;
+#pragma unroll
+  for (int m = 0; m < M; ++m) c[m] = (uint32_t)(v >> (m * B)) & code_mask(B);
+}
+
 __device__ __forceinline__ void unpack8(const uint4& v, float (&f)[8]) {
   f[0] = h2f(v.x & 0xFFFF); f[1] = h2f(v.x >> 16);
   f[2] = h2f(v.y & 0xFFFF); f[3] = h2f(v.y >> 16);
@@ -54,10 +69,10 @@ __device__ __forceinline__ void unpack8(const uint4& v, float (&f)[8]) {
   f[6] = h2f(v.w & 0xFFFF); f[7] = h2f(v.w >> 16);
 }
 
-template <int M, int B>
+template <int M, int B, bool PACKED>
 __global__ __launch_bounds__(256) void k_dequant(const void* __restrict__ codes, const uint4* __restrict__ cb,
                                                  const uint16_t* __restrict__ scales, uint32_t total_groups,
-                                                 uint32_t G, uint4* __restrict__ w) {
+                                                 uint32_t G, uint32_t pwords, uint4* __restrict__ w) {
 #pragma clang fp contract(off)
   constexpr int kLdsEntries = (B == 8) ? M * 256 : 1;
   __shared__ uint4 cb_lds[kLdsEntries];
@@ -70,7 +85,10 @@ __global__ __launch_bounds__(256) void k_dequant(const void* __restrict__ codes,
     const uint32_t row = q / G;
     const float s = h2f(scales[row]);
     uint32_t c[M];
-    load_group_codes<M, B>(codes, q, c);
+    if constexpr (PACKED)
+      load_group_codes_packed<M, B>(static_cast<const uint32_t*>(codes) + (size_t)row * pwords, q - row * G, c);
+    else
+      load_group_codes<M, B>(codes, q, c);
     float acc[8];
     unpack8((B == 8) ? cb_lds[c[0]] : cb[c[0]], acc);
 #pragma unroll
@@ -94,19 +112,26 @@ __global__ __launch_bounds__(256) void k_dequant(const void* __restrict__ codes,
   }
 }
 
-template <int M, int B>
+template <int M, int B, bool PACKED = false>
 static hipError_t run_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
   const uint32_t total = (uint32_t)L.d_out * (uint32_t)L.G;
   uint32_t blocks = (total + 255u) / 256u;
   const uint32_t cap = (uint32_t)num_cus() * 8u;
   if (blocks > cap) blocks = cap;
-  hipLaunchKernelGGL((k_dequant<M, B>), dim3(blocks), dim3(256), 0, s, L.codes,
-                     reinterpret_cast<const uint4*>(L.codebooks), L.scales, total, (uint32_t)L.G,
+  const uint32_t pwords = PACKED ? (uint32_t)packed_row_words(L.G, M, B) : 0u;
+  hipLaunchKernelGGL((k_dequant<M, B, PACKED>), dim3(blocks), dim3(256), 0, s, L.codes,
+                     reinterpret_cast<const uint4*>(L.codebooks), L.scales, total, (uint32_t)L.G, pwords,
                      reinterpret_cast<uint4*>(w));
   return hipGetLastError();
 }
 
 hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s) {
+  if (L.packed) {
+    if (L.M == 1 && L.B == 15) return run_dequant<1, 15, true>(L, w, s);
+    if (L.M == 2 && L.B == 12) return run_dequant<2, 12, true>(L, w, s);
+    if (L.M == 2 && L.B == 15) return run_dequant<2, 15, true>(L, w, s);
+    return hipErrorInvalidValue;
+  }
   if (L.B > 8) {
     if (L.M == 1) return L.B == 16 ? run_dequant<1, 16>(L, w, s) : run_dequant<1, 15>(L, w, s);
     switch (L.B) {

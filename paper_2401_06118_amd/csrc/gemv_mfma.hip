@@ -20,8 +20,12 @@
 //     codebooks (128 KiB);
 //   k_gemv_ks (B = 8): each wave owns whole K-slices of all the workgroup's
 //     row blocks and keeps one accumulator per block;
-//   k_gemv_cb (B = 16, large launches): the k_gemv_ks split with the codes
-//     held in registers, run once per 128 KiB codebook chunk staged in LDS.
+//   k_gemv_cb (one codebook of 15- or 16-bit codes, large launches): the
+//     k_gemv_ks split with the codes held in registers, run once per 128 KiB
+//     codebook chunk staged in LDS.
+// k_gemv_mfma and k_gemv_cb also read bit-packed codes (B bits per code, a
+// bit string per row): a lane loads the 3 or 5 dwords that hold its slot's 8
+// codes and cuts them out with shifts.
 // In every case the per-wave partials are added in a fixed order at the end,
 // so results are deterministic.
 //
@@ -50,9 +54,14 @@ constexpr int kWaves = 16;
 constexpr int kThreads = kWaves * kWave;
 constexpr int kMaxRB = 8;  // 16-row blocks per workgroup
 
-template <int M, int B, int COPIES, int PF, bool VEC>
+// PACKED: bit-packed B-bit codes (B = 12 or 15), a slot's 8 codes cut out of
+// the 3 (B = 12) or 5 (B = 15) 32-bit words that hold them; a slot of 15-bit
+// codes starts 24 * slot % 32 bits into its first word.
+template <int M, int B, int COPIES, int PF, bool VEC, bool PACKED = false>
 __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
   using C = GCfg<B>;
+  static_assert(!PACKED || B == 12 || B == 15, "packed codes: 12 or 15 bits");
+  constexpr int kW = PACKED ? (B == 12 ? 3 : 5) : 4;  // code words per slot
   extern __shared__ uint4 lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -78,7 +87,8 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
   // Items are dealt round-robin: wave w takes items w, w + 16, w + 32, ...
   // (nk of them); item i covers row block i / KS and K-slice i % KS.
   const int nk = items > wave ? (items - wave + kWaves - 1) / kWaves : 0;
-  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * pitch;
+  const uint32_t pwords = (uint32_t)bt.p[p].pwords;  // packed: 32-bit words per row
+  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * (PACKED ? pwords * 4u : pitch);
 
   // Wide codes with COPIES = 1: the M codebooks sit whole in LDS, one copy
   // (two 4096-entry codebooks are 128 KiB).
@@ -116,11 +126,34 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
   // the wave's last item, so loads past the end repeat that item (valid
   // memory; their results are never used).
   const uint32_t slot_off = (uint32_t)slot * 16u;
-  auto issue = [&](int rb, int ks, uint32_t (&w)[4]) {
+  auto issue = [&](int rb, int ks, uint32_t (&w)[kW]) {
     int row = rb * 16 + r16;
     row = row < rows ? row : rows - 1;
     const uint32_t off = (uint32_t)ks * 64u + slot_off;
-    if constexpr (VEC) {
+    if constexpr (PACKED) {
+      // words of codes 8 * (4 ks + slot) .. + 7, as one 12-byte load (B = 12)
+      // or a 16-byte and a 4-byte load (B = 15), dword-aligned; at the end
+      // of a row the words past its last are clamped to it, one by one (those
+      // codes meet x = 0)
+      const uint32_t* rw = reinterpret_cast<const uint32_t*>(wg_codes) + (size_t)row * pwords;
+      const uint32_t w0 = ((uint32_t)(ks * 4 + slot) * 8u * (uint32_t)B) >> 5;
+      if (w0 + (uint32_t)kW <= pwords) {
+        if constexpr (B == 12) {
+          const u32x3a4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x3a4_t*>(rw + w0));
+          w[0] = v[0]; w[1] = v[1]; w[2] = v[2];
+        } else {
+          const u32x4a4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4a4_t*>(rw + w0));
+          w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
+          w[4] = __builtin_nontemporal_load(rw + w0 + 4);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < kW; ++i) {
+          const uint32_t wi = w0 + (uint32_t)i < pwords ? w0 + (uint32_t)i : pwords - 1u;
+          w[i] = __builtin_nontemporal_load(rw + wi);
+        }
+      }
+    } else if constexpr (VEC) {
       // a 16-byte slot is wholly inside the row or wholly past its end
       const uint32_t o = (uint32_t)row * pitch + (off < pitch ? off : 0u);
       const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
@@ -134,7 +167,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
     while (ks >= KS) { ks -= KS; ++rb; }
   };
   int f_rb = nk > 0 ? wave / KS : 0, f_ks = nk > 0 ? wave % KS : 0, f_k = 0;
-  uint32_t buf[PF][4];
+  uint32_t buf[PF][kW];
 #pragma unroll
   for (int u = 0; u < PF; ++u) {
     issue(f_rb, f_ks, buf[u]);
@@ -179,7 +212,31 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
       const int k = k0 + u;
-      const uint32_t cw[4] = {buf[u][0], buf[u][1], buf[u][2], buf[u][3]};
+      // the slot's 8 codes: 16-bit lanes of 4 words, or a packed bit string
+      // (shifted to start at bit 0)
+      uint32_t cw[4];
+      if constexpr (!PACKED) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cw[i] = buf[u][i];
+      } else if constexpr (B == 12) {
+#pragma unroll
+        for (int i = 0; i < 3; ++i) cw[i] = buf[u][i];
+        cw[3] = 0;
+      } else {
+        const uint32_t sh = (24u * (uint32_t)slot) & 31u;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cw[i] = __builtin_amdgcn_alignbit(buf[u][i + 1], buf[u][i], sh);
+      }
+      auto code_of = [&](int t) -> uint32_t {
+        if constexpr (PACKED) {
+          const int b = t * B, wd = b >> 5, of = b & 31;
+          uint32_t v = cw[wd] >> of;
+          if (of + B > 32) v |= cw[wd + 1] << (32 - of);
+          return v & code_mask(B);
+        } else {
+          return (cw[t / 2] >> (16 * (t % 2))) & code_mask(B);
+        }
+      };
       uint4 av[C::kCPL];
       if constexpr (B > 8 && !kWideLds) {
         // L2 gathers go out before the next code load so that waiting for
@@ -188,9 +245,8 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
         if (k < nk) {
 #pragma unroll
           for (int t = 0; t < C::kCPL; ++t)
-            av[t] = *reinterpret_cast<const uint4*>(
-                reinterpret_cast<const char*>(cb) + ((uint32_t)(t % M) << (B + 4)) +
-                (((cw[t / 2] >> (16 * (t % 2))) & code_mask(B)) << 4));
+            av[t] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb) +
+                                                    ((uint32_t)(t % M) << (B + 4)) + (code_of(t) << 4));
         }
       }
       issue(f_rb, f_ks, buf[u]);
@@ -221,8 +277,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
 #pragma unroll
             for (int uu = 0; uu < 4; ++uu) {
               const int t = t0 + uu;
-              av[t] = lds_load16(cb_base + ((uint32_t)(t % M) << (B + 4)) +
-                                 (((cw[t / 2] >> (16 * (t % 2))) & code_mask(B)) << 4));
+              av[t] = lds_load16(cb_base + ((uint32_t)(t % M) << (B + 4)) + (code_of(t) << 4));
             }
           }
 #pragma unroll
@@ -535,8 +590,11 @@ __device__ __forceinline__ void cb_chunk_addr(uint32_t word, uint32_t first2, ui
   asm("v_mad_u32_u16 %0, %1, 16, %2 op_sel:[1,0,0,0]" : "=v"(a1) : "v"(tw), "v"(base));
 }
 
-template <int NKS, int RB, int B>
+// PACKED (B = 15): the codes arrive as row bit strings; each item's 8 codes
+// per lane are unpacked once into the 16-bit pairs the passes read.
+template <int NKS, int RB, int B, bool PACKED = false>
 __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
+  static_assert(!PACKED || B == 15, "packed codes: 15 bits");
   constexpr int kCbPasses = cb_passes(B);
   static_assert(kCbPasses * kCbChunk == (1 << B), "whole chunks");
   constexpr int kItems = NKS * RB;
@@ -560,8 +618,9 @@ __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
   int32_t rows = bt.p[p].d_out - row0;
   if (rows > rows_per_wg) rows = rows_per_wg;
   const int32_t G = bt.p[p].G;
-  const uint32_t pitch = (uint32_t)G * 2u;  // code bytes per row
-  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * pitch;
+  const uint32_t pitch = (uint32_t)G * 2u;  // code bytes per row (unpacked)
+  const uint32_t pwords = (uint32_t)bt.p[p].pwords;  // packed: 32-bit words per row
+  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * (PACKED ? pwords * 4u : pitch);
 
   uint4* x_lds = lds + kCbChunk + 1;  // after the chunk and its zero codeword
 
@@ -584,16 +643,32 @@ __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
   // zero there.  Rows past the workgroup's last repeat that row; their sums
   // are never stored.
   uint32_t cw[kItems][4];
+  uint32_t raw[PACKED ? kItems : 1][5];  // packed: the 5 words that hold a slot's 120 bits
 #pragma unroll
   for (int j = 0; j < NKS; ++j) {
     const uint32_t off = (uint32_t)(wave + j * kWaves) * 64u + (uint32_t)slot * 16u;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
       const int row = rb * 16 + r16 < rows ? rb * 16 + r16 : rows - 1;
-      const uint32_t o = (uint32_t)row * pitch + (off < pitch ? off : 0u);
-      const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
+      if constexpr (PACKED) {
+        // words past the row's last are clamped to it (x is zero there)
+        const uint32_t* rw = reinterpret_cast<const uint32_t*>(wg_codes) + (size_t)row * pwords;
+        const uint32_t w0 = ((uint32_t)((wave + j * kWaves) * 4 + slot) * 120u) >> 5;
+        uint32_t* r = raw[j * RB + rb];
+        if (w0 + 5u <= pwords) {
+          const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4a4_t*>(rw + w0));
+          r[0] = v[0]; r[1] = v[1]; r[2] = v[2]; r[3] = v[3];
+          r[4] = __builtin_nontemporal_load(rw + w0 + 4);
+        } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) cw[j * RB + rb][e] = v[e];
+          for (int i = 0; i < 5; ++i) r[i] = __builtin_nontemporal_load(rw + (w0 + i < pwords ? w0 + i : pwords - 1u));
+        }
+      } else {
+        const uint32_t o = (uint32_t)row * pitch + (off < pitch ? off : 0u);
+        const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) cw[j * RB + rb][e] = v[e];
+      }
     }
   }
   const uint16_t sc = bt.p[p].scales[row0 + (tid < rows ? tid : rows - 1)];
@@ -620,6 +695,30 @@ __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
     if (c + 1 < kCbPasses) {
 #pragma unroll
       for (int k = 0; k < kCbStage; ++k) stage[k] = cbv[(c + 1) * kCbChunk + tid + k * kThreads];
+    }
+    if constexpr (PACKED) {
+      // unpack the codes once, after the next chunk's loads are issued (so
+      // that those need not wait for the codes); a slot's bits start
+      // 24 * slot % 32 bits into its first word
+      if (c == 0) {
+        const uint32_t sh = (24u * (uint32_t)slot) & 31u;
+#pragma unroll
+        for (int it = 0; it < kItems; ++it) {
+          uint32_t w[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) w[i] = __builtin_amdgcn_alignbit(raw[it][i + 1], raw[it][i], sh);
+          uint32_t code[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) {
+            const int b = t * 15, wd = b >> 5, of = b & 31;
+            uint32_t v = w[wd] >> of;
+            if (of + 15 > 32) v |= w[wd + 1] << (32 - of);
+            code[t] = v & 0x7FFFu;
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cw[it][e] = code[2 * e] | (code[2 * e + 1] << 16);
+        }
+      }
     }
     const uint32_t first2 = (uint32_t)(c * kCbChunk) * 0x10001u;
 #pragma unroll
@@ -700,9 +799,9 @@ __global__ __launch_bounds__(kThreads) void k_gemv_cb(const GemvBatch bt) {
   }
 }
 
-template <int NKS, int RB, int B>
+template <int NKS, int RB, int B, bool PACKED>
 hipError_t launch_cb(const GemvBatch& bt, hipStream_t s) {
-  auto kern = k_gemv_cb<NKS, RB, B>;
+  auto kern = k_gemv_cb<NKS, RB, B, PACKED>;
   {
     const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), 160 * 1024);
     if (e != hipSuccess) return e;
@@ -718,21 +817,21 @@ hipError_t launch_cb(const GemvBatch& bt, hipStream_t s) {
 constexpr int kCbMaxNks = 3;
 constexpr int cb_rb_cap(int nks) { return nks == 1 ? 6 : (nks == 2 ? 4 : 2); }
 
-template <int B>
+template <int B, bool PACKED = false>
 hipError_t launch_cb_shape(const GemvBatch& bt, int nks, int rb, hipStream_t s) {
   switch (nks * 8 + rb) {
-    case 8 + 1: return launch_cb<1, 1, B>(bt, s);
-    case 8 + 2: return launch_cb<1, 2, B>(bt, s);
-    case 8 + 3: return launch_cb<1, 3, B>(bt, s);
-    case 8 + 4: return launch_cb<1, 4, B>(bt, s);
-    case 8 + 5: return launch_cb<1, 5, B>(bt, s);
-    case 8 + 6: return launch_cb<1, 6, B>(bt, s);
-    case 16 + 1: return launch_cb<2, 1, B>(bt, s);
-    case 16 + 2: return launch_cb<2, 2, B>(bt, s);
-    case 16 + 3: return launch_cb<2, 3, B>(bt, s);
-    case 16 + 4: return launch_cb<2, 4, B>(bt, s);
-    case 24 + 1: return launch_cb<3, 1, B>(bt, s);
-    case 24 + 2: return launch_cb<3, 2, B>(bt, s);
+    case 8 + 1: return launch_cb<1, 1, B, PACKED>(bt, s);
+    case 8 + 2: return launch_cb<1, 2, B, PACKED>(bt, s);
+    case 8 + 3: return launch_cb<1, 3, B, PACKED>(bt, s);
+    case 8 + 4: return launch_cb<1, 4, B, PACKED>(bt, s);
+    case 8 + 5: return launch_cb<1, 5, B, PACKED>(bt, s);
+    case 8 + 6: return launch_cb<1, 6, B, PACKED>(bt, s);
+    case 16 + 1: return launch_cb<2, 1, B, PACKED>(bt, s);
+    case 16 + 2: return launch_cb<2, 2, B, PACKED>(bt, s);
+    case 16 + 3: return launch_cb<2, 3, B, PACKED>(bt, s);
+    case 16 + 4: return launch_cb<2, 4, B, PACKED>(bt, s);
+    case 24 + 1: return launch_cb<3, 1, B, PACKED>(bt, s);
+    case 24 + 2: return launch_cb<3, 2, B, PACKED>(bt, s);
   }
   return hipErrorInvalidValue;
 }
@@ -790,9 +889,9 @@ hipError_t launch_ks_rb(const GemvBatch& bt, int rb, int nks, size_t lds_bytes, 
   return hipErrorInvalidValue;
 }
 
-template <int M, int B, int COPIES, int PF, bool VEC>
+template <int M, int B, int COPIES, int PF, bool VEC, bool PACKED = false>
 hipError_t launch_pf(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
-  auto kern = k_gemv_mfma<M, B, COPIES, PF, VEC>;
+  auto kern = k_gemv_mfma<M, B, COPIES, PF, VEC, PACKED>;
   {
     const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), 160 * 1024);
     if (e != hipSuccess) return e;
@@ -801,12 +900,12 @@ hipError_t launch_pf(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int M, int B, int COPIES, bool VEC>
+template <int M, int B, int COPIES, bool VEC, bool PACKED = false>
 hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStream_t s) {
   switch (pf) {
-    case 1: return launch_pf<M, B, COPIES, 1, VEC>(bt, lds_bytes, s);
-    case 2: return launch_pf<M, B, COPIES, 2, VEC>(bt, lds_bytes, s);
-    case 4: return launch_pf<M, B, COPIES, 4, VEC>(bt, lds_bytes, s);
+    case 1: return launch_pf<M, B, COPIES, 1, VEC, PACKED>(bt, lds_bytes, s);
+    case 2: return launch_pf<M, B, COPIES, 2, VEC, PACKED>(bt, lds_bytes, s);
+    case 4: return launch_pf<M, B, COPIES, 4, VEC, PACKED>(bt, lds_bytes, s);
   }
   return hipErrorInvalidValue;
 }
@@ -840,6 +939,9 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
                             hipStream_t s) {
   if (count < 1 || count > kMaxProblems) return hipErrorInvalidValue;
   const int M = Ls[0].M, B = Ls[0].B;
+  const bool packed = Ls[0].packed;
+  for (int i = 1; i < count; ++i)
+    if (Ls[i].packed != packed) return hipErrorInvalidValue;
   const int kCPL = (B == 8) ? 16 : 8, kKS = 4 * kCPL;
   bool vec = true;
   double total_bytes = 0;
@@ -926,6 +1028,7 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     P.G = L.G;
     P.wg_begin = wg;
     P.rows_per_wg = rows_per_wg;
+    P.pwords = packed ? packed_row_words(L.G, M, B) : 0;
     wg += nwg;
     if (ni > ni_max) ni_max = ni;
     const int xg = KS * (kKS / M);
@@ -941,8 +1044,20 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   if (xg_max > xl * kThreads) return hipErrorInvalidValue;
   const size_t base = (size_t)xg_max * 16 + (size_t)rb_max * kWaves * 16 * 4;
   const size_t limit = 160 * 1024;
-  if (B > 8 && cb_nks > 0)
+  if (B > 8 && cb_nks > 0) {
+    if (packed) return launch_cb_shape<15, true>(bt, cb_nks, rb_max, s);
     return B == 15 ? launch_cb_shape<15>(bt, cb_nks, rb_max, s) : launch_cb_shape<16>(bt, cb_nks, rb_max, s);
+  }
+  if (packed) {
+    if (base > limit) return hipErrorInvalidValue;
+    const size_t wide12 = (size_t)(2 << 12) * 16;
+    if (M == 2 && B == 12 && base + wide12 <= limit)
+      return launch_copies<2, 12, 1, true, true>(bt, ni, base + wide12, s);
+    if (M == 2 && B == 12) return launch_copies<2, 12, 0, true, true>(bt, ni, base, s);
+    if (M == 2 && B == 15) return launch_copies<2, 15, 0, true, true>(bt, ni, base, s);
+    if (M == 1 && B == 15) return launch_copies<1, 15, 0, true, true>(bt, ni, base, s);
+    return hipErrorInvalidValue;
+  }
   if (B > 8) {
     if (base > limit) return hipErrorInvalidValue;
 #define AQLM_GEMV_L2(MM, BB) \

@@ -18,6 +18,9 @@ constexpr bool format_supported(int M, int B) {
          ((B == 12 || B == 15 || B == 16) && M == 2);
 }
 
+// Bit-packed codes: 12-bit codes of two codebooks, 15-bit codes of one or two.
+constexpr bool packed_supported(int M, int B) { return (B == 12 && M == 2) || (B == 15 && (M == 1 || M == 2)); }
+
 struct Layer {
   const void* codes;          // [d_out][G][M] uint8 (B = 8) or uint16 (B > 8)
   const uint16_t* codebooks;  // [M][2^B][8] fp16
@@ -28,7 +31,13 @@ struct Layer {
   int32_t M;
   int32_t B;
   bool vec_codes;  // codes base 16-byte aligned and row pitch a multiple of 16 bytes
+  bool packed;     // B-bit codes packed into a bit string per row (32-bit words; B = 12, 15)
 };
+
+// 32-bit words of one row of packed codes: G*M codes of B bits, zero-padded.
+inline int32_t packed_row_words(int32_t G, int32_t M, int32_t B) {
+  return (int32_t)(((int64_t)G * M * B + 31) / 32);
+}
 
 constexpr int kMaxProblems = 8;
 
@@ -44,6 +53,7 @@ struct GemvProblem {
   int32_t G;
   int32_t wg_begin;
   int32_t rows_per_wg;
+  int32_t pwords;  // packed codes: 32-bit words per row (0: unpacked)
 };
 
 struct GemvBatch {

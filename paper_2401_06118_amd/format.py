@@ -42,6 +42,15 @@ class AqlmShape:
         B <= 8, two for 8 < B <= 16 (unpacked, no padding)."""
         return self.d_out * self.groups * self.code_bytes_per_group
 
+    def packed_codes_bytes(self) -> int:
+        """Bytes of the bit-packed code tensor: B bits per code, each row padded
+        to whole 32-bit words."""
+        return self.d_out * packed_row_bytes(self.d_in, self.M, self.B, self.g)
+
+    def packed_gemv_bytes(self, n: int = 1) -> int:
+        """:meth:`gemv_bytes` with bit-packed codes."""
+        return self.gemv_bytes(n) - self.codes_bytes() + self.packed_codes_bytes()
+
     def codebook_bytes(self) -> int:
         return self.M * (1 << self.B) * self.g * 2
 

@@ -136,3 +136,20 @@ def device_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, n
     scales = torch.empty(d_out, device=device).uniform_(0.5, 1.5, generator=gen).to(torch.float16)
     x = torch.randn((n, d_in), device=device, generator=gen).to(torch.float16)
     return codes, codebooks, scales, x
+
+
+def device_packed_layer(seed: int, d_out: int, d_in: int, M: int, B: int, g: int = 8, n: int = 1,
+                        device="cuda", cb_std: float = 0.02):
+    """:func:`device_layer` with bit-packed codes: uniformly random 32-bit
+    words (every B-bit field of them is a uniform code), int32
+    [d_out, ceil(d_in/g * M * B / 32)]."""
+    import torch
+
+    _, codebooks, scales, x = device_layer(seed, 8, d_in, M, B, g, n, device, cb_std)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed + 1)
+    words = ((d_in // g) * M * B + 31) // 32
+    codes = torch.randint(-(1 << 31), 1 << 31, (d_out, words), dtype=torch.int64, device=device,
+                          generator=gen).to(torch.int32)
+    scales = torch.empty(d_out, device=device).uniform_(0.5, 1.5, generator=gen).to(torch.float16)
+    return codes, codebooks, scales, x

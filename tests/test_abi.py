@@ -18,7 +18,7 @@ P = 0x10000  # a 64 KiB-aligned fake device address; never dereferenced on error
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^(?:int|size_t|const char\*)\s+(aqlm_\w+)\s*\(", text, flags=re.M)))
+    return sorted(set(re.findall(r"^(?:int|int64_t|size_t|const char\*)\s+(aqlm_\w+)\s*\(", text, flags=re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -218,3 +218,53 @@ def test_beam_search_refuses_before_launch(lib):
     assert call(beam=9) == UNSUP
     assert call(d_in=4096, beam=8) == UNSUP      # state beyond the on-chip budget
     assert call(w=P + 2) == ALIGN
+
+
+PACKED = _lib.PACKED
+
+
+def test_packed_row_words(lib):
+    # ceil(G * M * B / 32): 2x12 -> 3 words per 4 groups, 1x15 / 2x15 ragged
+    assert lib.aqlm_packed_row_words(4096, 2, 12, 8) == 4096 // 8 * 24 // 32
+    assert lib.aqlm_packed_row_words(4096, 2, 12 | PACKED, 8) == 384
+    assert lib.aqlm_packed_row_words(8, 1, 15, 8) == 1
+    assert lib.aqlm_packed_row_words(24, 1, 15, 8) == 2
+    assert lib.aqlm_packed_row_words(8008, 2, 15, 8) == (1001 * 30 + 31) // 32
+    assert lib.aqlm_packed_row_words(0, 2, 12, 8) == 0
+
+
+def test_packed_codes_accepted_only_where_supported(lib):
+    """Packed codes: 2x12, 2x15 and 1x15 pass the checks of dequantize and
+    gemv (the calls then fail only on the fake pointers' alignment); every
+    other format, and every other entry point, refuses them."""
+    for M, B in ((2, 12), (2, 15), (1, 15)):
+        assert deq(lib, M=M, B=B | PACKED, w=P + 2) == ALIGN
+        assert gemv(lib, M=M, B=B | PACKED, y=P + 2) == ALIGN
+        assert gemm(lib, M=M, B=B | PACKED) == UNSUP
+        assert gemm_ws(lib, M=M, B=B | PACKED) == UNSUP
+    for M, B in ((2, 8), (1, 16), (2, 16), (4, 8), (1, 12)):
+        assert deq(lib, M=M, B=B | PACKED) == UNSUP
+        assert gemv(lib, M=M, B=B | PACKED) == UNSUP
+    # x beyond the matrix-core kernel's staging: no packed fallback
+    assert gemv(lib, d_in=8 * 16400, M=1, B=15 | PACKED) == UNSUP
+
+
+def test_packed_codes_refused_by_other_entry_points(lib):
+    p, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+    assert lib.aqlm_gemm_noalloc(P, P, P, 64, 64, 2, 12 | PACKED, 8, 4, P, P, None) == UNSUP
+    assert lib.aqlm_backward(P, P, P, 64, 64, 2, 12 | PACKED, 8, 4, P, P, P, P, None) == UNSUP
+    assert lib.aqlm_beam_search(P, P, P, P, P, 8, 64, 2, 12 | PACKED, 8, 4, 1, P, None) == UNSUP
+    Prob = _lib.GemvProblem
+    arr = (Prob * 1)(Prob(P, P, P, P, P, 64, 64))
+    assert lib.aqlm_gemv_grouped_path(arr, 1, 2, 12 | PACKED, 8, _lib.PATH_TABLE, None) == UNSUP
+    assert lib.aqlm_gemv_grouped_path(arr, 1, 2, 8 | PACKED, 8, _lib.PATH_GATHER, None) == UNSUP
+
+
+def test_binding_checks_packed_shapes():
+    import torch
+    import paper_2401_06118_amd as aq
+    cb = torch.zeros((2, 4096, 8), dtype=torch.float16)
+    sc = torch.ones(4, dtype=torch.float16)
+    words = torch.zeros((4, 3), dtype=torch.int32)
+    with pytest.raises(ValueError):
+        aq.packed_layer_args(words, cb, sc, 32)  # CPU tensors

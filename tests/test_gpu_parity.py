@@ -925,3 +925,108 @@ def test_2x12_high_code_bits_are_ignored():
     assert torch.equal(y.view(torch.int16), y_hi.view(torch.int16))
     assert torch.equal(yb.view(torch.int16), yb_hi.view(torch.int16))
     assert torch.equal(w.view(torch.int16), w_hi.view(torch.int16))
+
+
+# ------------------------------------------------ bit-packed 12- and 15-bit codes
+# (the code storage the paper's bits-per-parameter figures count: each row a
+# bit string of its d_in/8 * M codes, padded to whole 32-bit words)
+
+from paper_2401_06118_amd import format as aqfmt  # noqa: E402
+
+PACKED_FORMATS = [(2, 12), (2, 15), (1, 15)]
+
+
+def packed_device(lay):
+    """(int32 packed words, codebooks, scales, x) on the GPU; the words are
+    written by format.pack_codes on the host."""
+    _, cb, sc, x = to_device(lay)
+    B = int(lay.codebooks.shape[1]).bit_length() - 1
+    words = aqfmt.pack_codes(lay.codes, B).view(np.int32)
+    return torch.from_numpy(np.ascontiguousarray(words)).cuda(), cb, sc, x
+
+
+@pytest.mark.parametrize("M,B", PACKED_FORMATS)
+@pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (1000, 4104), (37, 8), (33, 8008), (5, 11008)])
+def test_packed_dequantize_bit_exact(M, B, d_out, d_in):
+    """Row bit strings whose groups straddle 32-bit words (15-bit codes) and
+    rows that end inside a word (ragged G * M * B)."""
+    print(f"[packed dequant] {M}x{B} {d_out}x{d_in}", flush=True)
+    lay = synth.layer(19_000 + 7 * B + d_out + d_in, d_out, d_in, M, B)
+    words, cb, sc, _ = packed_device(lay)
+    w = aq().dequantize(words, cb, sc, d_in=d_in)
+    torch.cuda.synchronize()
+    assert_bits_equal(w.cpu().numpy().view(np.uint16),
+                      oracle.dequantize_packed(aqfmt.pack_codes(lay.codes, B), lay.codebooks, lay.scales, d_in, B),
+                      "packed dequantize")
+
+
+@pytest.mark.parametrize("M,B", PACKED_FORMATS)
+@pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (11008, 4096), (4096, 11008), (1000, 4104), (37, 8),
+                                        (33, 8008), (4000, 8008), (64, 16384), (24, 65536)])
+def test_packed_gemv_matches_oracle(M, B, d_out, d_in):
+    """The matrix-core kernel reading packed rows: 2x12 with the codebooks in
+    LDS (d_in up to 11008) and from L2, 2x15 from L2, 1x15 from L2 (small
+    launches) or through LDS chunk by chunk (the 11008 x 4096, 4096 x 11008
+    and 4000 x 8008 layers); ragged rows,
+    slots whose codes straddle words, and the largest x the kernel stages
+    (d_in = 65536; beyond it packed codes are refused).  Where the unpacked
+    codes take the same kernel (two codebooks, 16-byte code rows) the result
+    is bit for bit the unpacked one."""
+    print(f"[packed gemv] {M}x{B} {d_out}x{d_in}", flush=True)
+    lay = synth.layer(19_500 + 7 * B + d_out + d_in, d_out, d_in, M, B)
+    words, cb, sc, x = packed_device(lay)
+    y = aq().gemv(words, cb, sc, x[0])
+    codes, _, _, _ = to_device(lay)
+    y_unpacked = aq().gemv(codes, cb, sc, x[0])
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y)[None, :])
+    if M == 2 and ((d_in // 8) * M * 2) % 16 == 0:
+        assert torch.equal(y.view(torch.int16), y_unpacked.view(torch.int16))
+
+
+@pytest.mark.parametrize("M,B", PACKED_FORMATS)
+def test_packed_gemv_grouped_matches_oracle(M, B):
+    """q, k, v-shaped problems and a ragged one in one grouped launch."""
+    print(f"[packed grouped] {M}x{B}", flush=True)
+    shapes = [(4096, 4096), (1024, 4096), (1024, 4096), (77, 4104)] if M == 2 else \
+        [(4096, 4096), (300, 8008), (11008, 4096)]
+    lays = [synth.layer(20_000 + 13 * i + B, o, i_, M, B) for i, (o, i_) in enumerate(shapes)]
+    probs, ys = [], []
+    for lay in lays:
+        words, cb, sc, x = packed_device(lay)
+        y = torch.empty(lay.codes.shape[0], dtype=torch.float16, device="cuda")
+        probs.append((words, cb, sc, x[0], y))
+        ys.append(y)
+    aq().gemv_grouped(probs)
+    torch.cuda.synchronize()
+    for lay, y in zip(lays, ys):
+        check_products(lay, fp16_to_np(y)[None, :])
+
+
+def test_packed_gemv_deterministic():
+    lay = synth.layer(20_100, 2048, 4096, 2, 15)
+    words, cb, sc, x = packed_device(lay)
+    ys = [aq().gemv(words, cb, sc, x[0]).clone() for _ in range(10)]
+    torch.cuda.synchronize()
+    assert all(torch.equal(ys[0].view(torch.int16), y.view(torch.int16)) for y in ys[1:])
+
+
+def test_packed_codes_refused_where_unsupported():
+    """Entry points without a packed path refuse before launching; so do the
+    table path and aqlm_gemv when x does not fit the matrix-core kernel."""
+    lay = synth.layer(20_200, 64, 1024, 2, 12, n=4)
+    words, cb, sc, x = packed_device(lay)
+    for fn in (lambda: aq().gemm_small_batch(words, cb, sc, x),
+               lambda: aq().gemm(words, cb, sc, x)):
+        with pytest.raises((ValueError, aq().AqlmError)):
+            fn()
+    y = torch.zeros(64, dtype=torch.float16, device="cuda")
+    with pytest.raises(aq().AqlmError):
+        aq().gemv_grouped([(words, cb, sc, x[0], y)], path="table")
+    big = synth.layer(20_300, 4, 8 * 16400, 1, 15)
+    words, cb, sc, x = packed_device(big)
+    y = torch.zeros(4, dtype=torch.float16, device="cuda")
+    with pytest.raises(aq().AqlmError):
+        aq().gemv(words, cb, sc, x[0], out=y)
+    torch.cuda.synchronize()
+    assert not y.any()
