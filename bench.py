@@ -415,7 +415,8 @@ def single_layer_rows(aq, torch):
         pair_ms = sum(pair) / len(pair)
         del g
         b = shp.packed_gemv_bytes(1) if packed else shp.gemv_bytes(1)
-        rows.append({"layer": name, "bytes": b, "us_per_call": ms * 1e3, "frac_per_call": b / (ms * 1e6) / HBM_PEAK_GBS,
+        pb = shp.paper_gemv_bytes(1)  # codes at B bits each
+        rows.append({"layer": name, "bytes": b, "paper_bytes": pb, "GBs_paper_bytes": pb / (ms * 1e6), "us_per_call": ms * 1e3, "frac_per_call": b / (ms * 1e6) / HBM_PEAK_GBS,
                      "GBs_per_call": b / (ms * 1e6), "event_pair_us": pair_ms * 1e3,
                      "GBs_event_pair": b / (pair_ms * 1e6), "replicas": reps})
         del layers

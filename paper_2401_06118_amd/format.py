@@ -42,6 +42,15 @@ class AqlmShape:
         B <= 8, two for 8 < B <= 16 (unpacked, no padding)."""
         return self.d_out * self.groups * self.code_bytes_per_group
 
+    def paper_codes_bytes(self) -> int:
+        """Bytes of the codes at exactly B bits per code (the paper's storage
+        count, no padding): d_out * d_in/g * M * B / 8."""
+        return self.d_out * self.groups * self.M * self.B // 8
+
+    def paper_gemv_bytes(self, n: int = 1) -> int:
+        """:meth:`gemv_bytes` with the codes counted at B bits each."""
+        return self.gemv_bytes(n) - self.codes_bytes() + self.paper_codes_bytes()
+
     def packed_codes_bytes(self) -> int:
         """Bytes of the bit-packed code tensor: B bits per code, each row padded
         to whole 32-bit words."""
