@@ -25,7 +25,8 @@ Also reported on the same JSON line:
   cpu_baseline  the CPU oracle (dequantize + fp64 product) timed on the host
                 cores on a sample of the step's layers, scaled to the step,
                 with the CPU model and a one-thread time;
-  secondary     the Llama-2-7B steps in 2x8 and 1x16, single layers rotated
+  secondary     the same step as one persistent launch (aqlm_gemv_step), the
+                Llama-2-7B steps in 2x8 and 1x16, single layers rotated
                 over >= 1 GiB of replicas (so HBM, not the 256 MB MALL, is
                 measured), the small-batch / prefill products,
                 dequantization, the gradients through Eq. 2 and the Phase-1
@@ -610,6 +611,29 @@ def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False):
     return layers, launches, graph, ms, spread, step_bytes
 
 
+def persistent_step_row(layers, graph, aq, torch, steps, step_bytes, graph_ms):
+    """The same decode step as one persistent launch (aqlm_gemv_step): the
+    block's four dependency levels, one level barrier each, timed like the
+    graph; its outputs are compared bit for bit with the graph's."""
+    levels = []
+    for b in range(0, len(layers), 7):
+        q, k, v, o, gate, up, down = layers[b:b + 7]
+        levels += [[q.problem(), k.problem(), v.problem()], [o.problem()], [gate.problem(), up.problem()],
+                   [down.problem()]]
+    step = aq.DecodeStep(levels)
+    step.run()
+    step.status()
+    ys = [L.y.clone() for L in layers]
+    graph.replay()
+    torch.cuda.synchronize()
+    same = all(torch.equal(a.view(torch.int16), L.y.view(torch.int16)) for a, L in zip(ys, layers))
+    del ys
+    ms = time_steps(step.run, steps, 2)
+    step.status()
+    return {"ms_per_step": ms, "GBs": step_bytes / (ms * 1e6), "frac": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
+            "levels": len(levels), "launches": 1, "vs_graph": graph_ms / ms, "bit_identical_to_graph": same}
+
+
 def step_seed(M: int) -> int:
     return 1000 * (1 if M == 2 else 2)
 
@@ -715,11 +739,15 @@ def main():
             "source_digest": digest,
         },
     }
+    persistent = None
+    if not args.no_secondary:
+        persistent = persistent_step_row(layers, graph, aq, torch, max(5, args.steps // 2), step_bytes, ms)
+        log(f"{args.workload} as one persistent launch: {persistent['ms_per_step']:.4f} ms per step")
     del layers, launches, graph
     torch.cuda.empty_cache()
 
     if not args.no_secondary:
-        sec = {}
+        sec = {"persistent_step": persistent}
         for other in ("llama2-7b-2x8", "llama2-7b-1x16"):
             if other == args.workload:
                 continue
@@ -731,6 +759,7 @@ def main():
                    "tok_s_eq": 1000.0 / oms, "spread": osp, "event_pair_sum_ms": sum(pair),
                    "GBs_event_pair": ob / (sum(pair) * 1e6)}
             if oM == 2:
+                row["persistent_step"] = persistent_step_row(ol, og, aq, torch, max(5, args.steps // 2), ob, oms)
                 # the same step without grouping (224 single launches), and
                 # without the block's dependencies (8 independent GEMVs per launch)
                 g1 = graph_of([lambda L=L: L.gemv(aq) for L in ol])

@@ -78,7 +78,8 @@ enum aqlm_status {
   AQLM_ERR_ALIGN = 4,       /* a pointer breaks the alignment rule above */
   AQLM_ERR_HIP = 5,         /* the HIP runtime reported an error */
   AQLM_ERR_WORKSPACE = 6,   /* aqlm_gemm: workspace smaller than aqlm_gemm_workspace_bytes */
-  AQLM_ERR_SCRATCH = 7      /* aqlm_gemm_noalloc: the product needs more than its fixed scratch */
+  AQLM_ERR_SCRATCH = 7,     /* aqlm_gemm_noalloc: the product needs more than its fixed scratch */
+  AQLM_ERR_TIMEOUT = 8      /* aqlm_gemv_step_status: a level barrier gave up waiting */
 };
 
 /* OR into B to pass bit-packed codes (see "Bit-packed codes" above). */
@@ -270,6 +271,58 @@ int aqlm_beam_search(const float* w, const float* h, void* codes, const uint16_t
 int aqlm_gemm_noalloc(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                       int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
                       void* stream);
+
+/* ---------------------------------------------------------------- decode step
+ *
+ * The matrix-vector products of a whole decode step in ONE launch (the paper
+ * times end-to-end generation with the model's computational graph compiled,
+ * App. "End-to-End Inference Speed", Table 13; here the compiled form is a
+ * step plan run by a persistent kernel).  A step is a list of levels; a level
+ * is 1..AQLM_MAX_GROUPED independent products computed exactly as
+ * aqlm_gemv_grouped computes them.  Level l + 1 starts reading its x only
+ * after every product of level l has been written, so a level may read what
+ * earlier levels wrote (e.g. level l + 1's x is level l's y).  While the last
+ * workgroups finish a level, the others already load the next level's codes,
+ * codebooks and scales.  2x8 (M = 2, B = 8, g = 8) with d_in a multiple of 64
+ * and x within the matrix-core kernel's staging (d_in <= 32768); anything else
+ * returns AQLM_ERR_UNSUPPORTED. */
+#define AQLM_STEP_MAX_LEVELS 65536
+#define AQLM_STEP_SYNC_BYTES 256
+#define AQLM_STEP_DEFAULT_SPIN (1u << 20)
+
+/* Bytes a plan of `levels` levels takes (0 if levels is out of range). */
+int64_t aqlm_gemv_step_plan_bytes(int32_t levels);
+
+/* Builds a step plan in HOST memory `plan` (plan_bytes >= the size above):
+ * `problems` (host array) holds the levels' problems one level after the
+ * other, level_sizes[l] of them for level l.  Every problem is validated as
+ * aqlm_gemv_grouped validates it; nothing touches the GPU, and the plan holds
+ * the problems' device pointers, so those buffers must outlive it.  The
+ * caller copies the plan, as bytes, to DEVICE memory (16-byte aligned) for
+ * aqlm_gemv_step.  The work split is sized for the current device.  A plan
+ * smaller than needed: AQLM_ERR_WORKSPACE. */
+int aqlm_gemv_step_plan(const aqlm_gemv_problem* problems, const int32_t* level_sizes, int32_t levels,
+                        int32_t M, int32_t B, int32_t g, void* plan, int64_t plan_bytes);
+
+/* Runs a planned step: one cooperative launch of one workgroup per CU on
+ * `stream`.  plan_host: the host plan; plan_dev: its device copy.  sync:
+ * DEVICE memory of AQLM_STEP_SYNC_BYTES, 16-byte aligned, zero before its
+ * first use; the launch leaves it zero again (apart from the error flag after
+ * a timeout), so it can be reused by the next launch on the same stream, but
+ * launches that overlap must not share it.  Each level barrier polls at most
+ * spin_limit times (0: AQLM_STEP_DEFAULT_SPIN, seconds of waiting) and then
+ * sets the error flag; from then on every workgroup stops at its next level
+ * barrier and the launch ends (outputs of the levels after the barrier that
+ * gave up are not written, or only partly).  Asynchronous like the
+ * other calls: check the flag with aqlm_gemv_step_status.  Returns
+ * AQLM_ERR_SHAPE for a plan made for a device with another CU count, and
+ * AQLM_ERR_HIP if the runtime refuses the cooperative launch. */
+int aqlm_gemv_step(const void* plan_host, const void* plan_dev, void* sync, uint32_t spin_limit, void* stream);
+
+/* Synchronizes `stream`, then reads and clears sync's error flag:
+ * AQLM_ERR_TIMEOUT if a level barrier of an earlier aqlm_gemv_step on it gave
+ * up, AQLM_OK otherwise. */
+int aqlm_gemv_step_status(void* sync, void* stream);
 
 /* Static text for a status code (never NULL). */
 const char* aqlm_status_string(int status);

@@ -12,7 +12,10 @@ Eq. 2 and Fig. 3).  This package exposes the three operations of the C ABI in
 - :func:`gemm` - that product with a workspace: for many rows the weights are
   dequantized once, then a dense fp16 matrix-core product reads them;
 - :func:`backward` - gradients of the codebooks and scales through Eq. 2;
-- :func:`beam_search` - Phase 1 of the quantizer: beam search over the codes.
+- :func:`beam_search` - Phase 1 of the quantizer: beam search over the codes;
+- :class:`DecodeStep` - the products of a whole decode step (levels of
+  grouped 2x8 products, each level free to read what earlier ones wrote) as
+  one persistent launch.
 
 Every computation runs in the hand-written HIP kernels of
 ``libaqlm_mi355x.so``; this module only marshals arguments.
@@ -33,7 +36,7 @@ from . import _lib
 from ._lib import AqlmError, status_string  # noqa: F401
 
 __all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "gemm_workspace_bytes", "gemm", "backward",
-           "beam_search",
+           "beam_search", "DecodeStep",
            "AqlmError",
            "status_string", "layer_args", "packed_layer_args"]
 
@@ -262,3 +265,66 @@ def beam_search(w, h, codes, codebooks, scales, *, beam: int, sweeps: int = 1, s
                                       loss.data_ptr(), _stream_handle(stream))
     _check(st, "aqlm_beam_search")
     return loss
+
+
+class DecodeStep:
+    """A planned decode step: ``levels`` is a list of levels, each a list of
+    (codes, codebooks, scales, x, y) 2x8 problems as for :func:`gemv_grouped`.
+    Level l + 1 reads its x only after level l has written every y, so a
+    level's x may be an earlier level's y.  The plan is built on the host,
+    copied to the device once, and :meth:`run` launches the whole step as one
+    persistent kernel.  The tensors must outlive the plan (it holds their
+    device pointers; references are kept here)."""
+
+    def __init__(self, levels, *, device=None):
+        import ctypes
+        if not levels:
+            raise ValueError("a step needs at least one level")
+        probs, sizes, keep = [], [], []
+        fmt = None
+        for lv in levels:
+            if not 1 <= len(lv) <= _lib.MAX_GROUPED:
+                raise ValueError(f"1..{_lib.MAX_GROUPED} problems per level")
+            sizes.append(len(lv))
+            for codes, codebooks, scales, x, y in lv:
+                d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)
+                if fmt is None:
+                    fmt = (M, B, g)
+                elif fmt != (M, B, g):
+                    raise ValueError("all problems of a step must share (M, B, g)")
+                if x.dtype != torch.float16 or x.numel() != d_in or not x.is_cuda or not x.is_contiguous():
+                    raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
+                if y.dtype != torch.float16 or y.numel() != d_out or not y.is_cuda or not y.is_contiguous():
+                    raise ValueError("y must be a contiguous fp16 GPU tensor with d_out elements")
+                probs.append(_lib.GemvProblem(codes.data_ptr(), codebooks.data_ptr(), scales.data_ptr(),
+                                              x.data_ptr(), y.data_ptr(), d_out, d_in))
+                keep.append((codes, codebooks, scales, x, y))
+        lib = _lib.load()
+        n = len(sizes)
+        nbytes = int(lib.aqlm_gemv_step_plan_bytes(n))
+        if nbytes <= 0:
+            raise ValueError("too many levels")
+        arr = (_lib.GemvProblem * len(probs))(*probs)
+        size_arr = (ctypes.c_int32 * n)(*sizes)
+        self._host = ctypes.create_string_buffer(nbytes)
+        st = lib.aqlm_gemv_step_plan(arr, size_arr, n, fmt[0], fmt[1], fmt[2], ctypes.addressof(self._host), nbytes)
+        _check(st, "aqlm_gemv_step_plan")
+        dev = keep[0][0].device if device is None else device
+        self._dev = torch.frombuffer(bytearray(self._host.raw), dtype=torch.uint8).to(dev)
+        self.sync = torch.zeros(_lib.STEP_SYNC_BYTES // 4, dtype=torch.int32, device=dev)
+        self._keep = keep
+        self.levels = n
+
+    def run(self, *, spin_limit: int = 0, stream=None):
+        """Launch the step (asynchronous); ``spin_limit`` bounds each level
+        barrier's polls (0: the library default)."""
+        import ctypes
+        st = _lib.load().aqlm_gemv_step(ctypes.addressof(self._host), self._dev.data_ptr(), self.sync.data_ptr(),
+                                        int(spin_limit), _stream_handle(stream))
+        _check(st, "aqlm_gemv_step")
+
+    def status(self, stream=None):
+        """Synchronize and raise AqlmError(AQLM_ERR_TIMEOUT) if a level barrier
+        of an earlier run gave up (the flag is cleared)."""
+        _check(_lib.load().aqlm_gemv_step_status(self.sync.data_ptr(), _stream_handle(stream)),
+               "aqlm_gemv_step_status")

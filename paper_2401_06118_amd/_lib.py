@@ -16,13 +16,16 @@ LIB_PATH = os.path.join(HERE, "libaqlm_mi355x.so")
 
 AQLM_OK = 0
 STATUS_NAMES = {0: "AQLM_OK", 1: "AQLM_ERR_NULL", 2: "AQLM_ERR_SHAPE", 3: "AQLM_ERR_UNSUPPORTED",
-                4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP", 6: "AQLM_ERR_WORKSPACE", 7: "AQLM_ERR_SCRATCH"}
+                4: "AQLM_ERR_ALIGN", 5: "AQLM_ERR_HIP", 6: "AQLM_ERR_WORKSPACE", 7: "AQLM_ERR_SCRATCH",
+                8: "AQLM_ERR_TIMEOUT"}
 PATH_AUTO, PATH_GATHER, PATH_TABLE = 0, 1, 2
 EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemv_grouped_path", "aqlm_gemm_small_batch",
            "aqlm_gemm_workspace_bytes", "aqlm_gemm", "aqlm_gemm_noalloc", "aqlm_backward", "aqlm_beam_search",
-           "aqlm_packed_row_words", "aqlm_status_string")
+           "aqlm_packed_row_words", "aqlm_gemv_step_plan_bytes", "aqlm_gemv_step_plan", "aqlm_gemv_step",
+           "aqlm_gemv_step_status", "aqlm_status_string")
 MAX_GROUPED = 8
 PACKED = 0x100  # OR-ed into B: bit-packed codes
+STEP_SYNC_BYTES = 256
 
 
 class GemvProblem(ctypes.Structure):
@@ -77,6 +80,15 @@ def load():
         lib.aqlm_beam_search.restype = ctypes.c_int
         lib.aqlm_packed_row_words.argtypes = [i64, i32, i32, i32]
         lib.aqlm_packed_row_words.restype = ctypes.c_int64
+        lib.aqlm_gemv_step_plan_bytes.argtypes = [i32]
+        lib.aqlm_gemv_step_plan_bytes.restype = ctypes.c_int64
+        lib.aqlm_gemv_step_plan.argtypes = [ctypes.POINTER(GemvProblem), ctypes.POINTER(ctypes.c_int32), i32, i32,
+                                            i32, i32, p, i64]
+        lib.aqlm_gemv_step_plan.restype = ctypes.c_int
+        lib.aqlm_gemv_step.argtypes = [p, p, p, ctypes.c_uint32, p]
+        lib.aqlm_gemv_step.restype = ctypes.c_int
+        lib.aqlm_gemv_step_status.argtypes = [p, p]
+        lib.aqlm_gemv_step_status.restype = ctypes.c_int
         lib.aqlm_status_string.argtypes = [ctypes.c_int]
         lib.aqlm_status_string.restype = ctypes.c_char_p
         _lib = lib

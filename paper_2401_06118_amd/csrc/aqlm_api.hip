@@ -352,6 +352,84 @@ int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int
   return AQLM_OK;
 }
 
+int64_t aqlm_gemv_step_plan_bytes(int32_t levels) {
+  if (levels < 1 || levels > AQLM_STEP_MAX_LEVELS) return 0;
+  return (int64_t)sizeof(aqlm::StepHeader) + (int64_t)levels * (int64_t)sizeof(aqlm::StepLevel);
+}
+
+int aqlm_gemv_step_plan(const aqlm_gemv_problem* problems, const int32_t* level_sizes, int32_t levels, int32_t M,
+                        int32_t B, int32_t g, void* plan, int64_t plan_bytes) {
+  if (!problems || !level_sizes || !plan) return AQLM_ERR_NULL;
+  if (levels < 1 || levels > AQLM_STEP_MAX_LEVELS) return AQLM_ERR_SHAPE;
+  if (plan_bytes < aqlm_gemv_step_plan_bytes(levels)) return AQLM_ERR_WORKSPACE;
+  auto* head = static_cast<aqlm::StepHeader*>(plan);
+  auto* lv = reinterpret_cast<aqlm::StepLevel*>(static_cast<char*>(plan) + sizeof(aqlm::StepHeader));
+  int32_t lds = 0;
+  int64_t first = 0;
+  for (int32_t l = 0; l < levels; ++l) {
+    const int32_t n = level_sizes[l];
+    if (n < 1 || n > AQLM_MAX_GROUPED) return AQLM_ERR_SHAPE;
+    aqlm::Layer Ls[AQLM_MAX_GROUPED];
+    const uint16_t* xs[AQLM_MAX_GROUPED];
+    uint16_t* ys[AQLM_MAX_GROUPED];
+    for (int32_t i = 0; i < n; ++i) {
+      const aqlm_gemv_problem& P = problems[first + i];
+      const int st = check_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &Ls[i]);
+      if (st != AQLM_OK) return st;
+      if (!P.x || !P.y) return AQLM_ERR_NULL;
+      if (!aligned(P.x, 16) || !aligned(P.y, 16)) return AQLM_ERR_ALIGN;
+      xs[i] = P.x;
+      ys[i] = P.y;
+    }
+    first += n;
+    // the step kernel carries the 2x8 matrix-core kernel with 16-byte code rows
+    if (M != 2 || B != 8) return AQLM_ERR_UNSUPPORTED;
+    for (int32_t i = 0; i < n; ++i)
+      if (!Ls[i].vec_codes) return AQLM_ERR_UNSUPPORTED;
+    if (!aqlm::gemv_mfma_fits(Ls, n)) return AQLM_ERR_UNSUPPORTED;
+    // as aqlm_gemv_grouped would launch it, or, where that layout is not in
+    // the step kernel (eight codebook copies with more than two row blocks),
+    // with at most two row blocks per workgroup
+    hipError_t e = aqlm::gemv_mfma_impl(Ls, xs, ys, n, nullptr, &lv[l], 0, aqlm::kStepLdsLimit);
+    if (e != hipSuccess) e = aqlm::gemv_mfma_impl(Ls, xs, ys, n, nullptr, &lv[l], 2, aqlm::kStepLdsLimit);
+    if (e != hipSuccess) return AQLM_ERR_UNSUPPORTED;
+    if (lv[l].lds_bytes > lds) lds = lv[l].lds_bytes;
+  }
+  head->magic = aqlm::kStepMagic;
+  head->levels = levels;
+  head->lds_bytes = lds;
+  head->grid = aqlm::num_cus();
+  return AQLM_OK;
+}
+
+int aqlm_gemv_step(const void* plan_host, const void* plan_dev, void* sync, uint32_t spin_limit, void* stream) {
+  if (!plan_host || !plan_dev || !sync) return AQLM_ERR_NULL;
+  const auto* head = static_cast<const aqlm::StepHeader*>(plan_host);
+  if (head->magic != aqlm::kStepMagic || head->levels < 1 || head->levels > AQLM_STEP_MAX_LEVELS)
+    return AQLM_ERR_SHAPE;
+  if (!aligned(plan_dev, 16) || !aligned(sync, 16)) return AQLM_ERR_ALIGN;
+  // (the workgroup split is sized for the device the plan was made on)
+  if (head->grid != aqlm::num_cus()) return AQLM_ERR_SHAPE;
+  const auto* lv = reinterpret_cast<const aqlm::StepLevel*>(static_cast<const char*>(plan_dev) +
+                                                             sizeof(aqlm::StepHeader));
+  const uint32_t spin = spin_limit ? spin_limit : AQLM_STEP_DEFAULT_SPIN;
+  return status_of(aqlm::launch_step(lv, head->levels, head->grid, (size_t)head->lds_bytes,
+                                     static_cast<uint32_t*>(sync), spin, static_cast<hipStream_t>(stream)));
+}
+
+int aqlm_gemv_step_status(void* sync, void* stream) {
+  if (!sync) return AQLM_ERR_NULL;
+  if (!aligned(sync, 16)) return AQLM_ERR_ALIGN;
+  if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return AQLM_ERR_HIP;
+  uint32_t err = 0;
+  uint32_t* flag = static_cast<uint32_t*>(sync) + 1;
+  if (hipMemcpy(&err, flag, sizeof(err), hipMemcpyDeviceToHost) != hipSuccess) return AQLM_ERR_HIP;
+  if (err == 0) return AQLM_OK;
+  const uint32_t zero = 0;
+  if (hipMemcpy(flag, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return AQLM_ERR_HIP;
+  return AQLM_ERR_TIMEOUT;
+}
+
 int64_t aqlm_packed_row_words(int64_t d_in, int32_t M, int32_t B, int32_t g) {
   if (d_in <= 0 || M <= 0 || B <= 0 || g <= 0) return 0;
   return ((d_in / g) * M * (int64_t)(B & ~AQLM_PACKED) + 31) / 32;
@@ -367,6 +445,7 @@ const char* aqlm_status_string(int status) {
     case AQLM_ERR_HIP: return "HIP runtime error";
     case AQLM_ERR_WORKSPACE: return "workspace too small";
     case AQLM_ERR_SCRATCH: return "needs more scratch than aqlm_gemm_noalloc's fixed buffer holds";
+    case AQLM_ERR_TIMEOUT: return "a decode-step level barrier timed out";
   }
   return "unknown status";
 }

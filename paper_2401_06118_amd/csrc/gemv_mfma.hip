@@ -317,8 +317,17 @@ __global__ __launch_bounds__(kThreads) void k_gemv_mfma(const GemvBatch bt) {
 // only), then runs the RB items (row blocks) of that slice, each into its own
 // accumulator, so no partial sums move until the end.  Code loads run
 // through a register ring of D K-slices, a few items ahead of their use.
-template <int M, int COPIES, int RB, int D, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
+//
+// The body serves two kernels: k_gemv_ks (one launch per grouped product;
+// vwg = blockIdx.x) and the persistent decode-step kernel k_gemv_step
+// (STEP = true), which runs many such products in a row on a resident grid.
+// With STEP, the code, codebook and scale loads of a product go out before
+// `wait()` (the level barrier: the previous product's outputs may be this
+// one's x), x is read after it with system-scope loads and y written with
+// system-scope stores (other workgroups of the same grid read it next, from
+// other XCDs); returns false when the wait gave up.
+template <int M, int COPIES, int RB, int D, bool VEC, bool STEP, typename Wait>
+__device__ __forceinline__ bool ks_body(const GemvBatch& bt, const int vwg, Wait&& wait) {
   using C = GCfg<8>;
   constexpr int kXS = C::kCPL / M;  // x slices per code slot per K-slice
   // codewords gathered per block before their MFMAs (fewer where the
@@ -350,11 +359,11 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   const int slot = lane >> 4;
 
   int p = 0;
-  while (p + 1 < bt.count && bt.p[p + 1].wg_begin <= (int)blockIdx.x) ++p;
+  while (p + 1 < bt.count && bt.p[p + 1].wg_begin <= vwg) ++p;
   const uint4* __restrict__ cb = bt.p[p].cb;
   const uint4* __restrict__ x = bt.p[p].x;
   const int32_t rows_per_wg = bt.p[p].rows_per_wg;
-  const int32_t row0 = ((int32_t)blockIdx.x - bt.p[p].wg_begin) * rows_per_wg;
+  const int32_t row0 = ((int32_t)vwg - bt.p[p].wg_begin) * rows_per_wg;
   int32_t rows = bt.p[p].d_out - row0;
   if (rows > rows_per_wg) rows = rows_per_wg;
   const int32_t G = bt.p[p].G;
@@ -368,6 +377,10 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   uint4* x_lds = lds + M * 256 * COPIES;
   float* part = reinterpret_cast<float*>(x_lds + bt.xg_max);
 
+  // (a persistent workgroup may still be reading the previous product's
+  // partial sums, which this one's staging can overlap)
+  if constexpr (STEP) __syncthreads();
+
   // 1. codebooks, x and scales first (they retire before the code stream).
   uint4 cbv = make_uint4(0, 0, 0, 0);
   if (tid < M * 256) cbv = cb[tid];
@@ -375,12 +388,25 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   // load of a clamped row, so that nothing waits for it here)
   const uint16_t sc = bt.p[p].scales[row0 + (tid < rows ? tid : rows - 1)];
   uint4 xv[C::kXL];
+  auto load_x = [&]() {
 #pragma unroll
-  for (int i = 0; i < C::kXL; ++i) {
-    const int grp = tid + i * kThreads;
-    xv[i] = make_uint4(0, 0, 0, 0);
-    if (grp < G) xv[i] = x[grp];
-  }
+    for (int i = 0; i < C::kXL; ++i) {
+      const int grp = tid + i * kThreads;
+      xv[i] = make_uint4(0, 0, 0, 0);
+      if (grp < G) {
+        if constexpr (STEP) {
+          const uint32_t* xw = reinterpret_cast<const uint32_t*>(x + grp);
+          xv[i].x = __hip_atomic_load(xw + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          xv[i].y = __hip_atomic_load(xw + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          xv[i].z = __hip_atomic_load(xw + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+          xv[i].w = __hip_atomic_load(xw + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        } else {
+          xv[i] = x[grp];
+        }
+      }
+    }
+  };
+  if constexpr (!STEP) load_x();
 
   // 2. code loads for the first kAhead items (rows past the end repeat the
   // last row; their sums are never stored).
@@ -406,6 +432,23 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
 #pragma unroll
   for (int i = 0; i < kAhead; ++i) issue_rb(i / RB, i % RB, ring[i / RB][i % RB]);
 
+  // (the step kernel: codebooks to LDS while waiting, then x)
+  auto stage_cb = [&]() {
+    constexpr bool kPair = COPIES == 8 && M == 2;
+    if (tid < M * 256) {
+#pragma unroll
+      for (int k = 0; k < COPIES; ++k) {
+        const int c = (k + lane) % COPIES;
+        cb_lds[kPair ? (tid & 255) * 16 + (tid >> 8) * 8 + c : tid * COPIES + c] = cbv;
+      }
+    }
+  };
+  if constexpr (STEP) {
+    stage_cb();
+    if (!wait()) return false;
+    load_x();
+  }
+
   // 3. stage codebook copies and x.  Eight copies of two codebooks (x too
   // large for sixteen) are interleaved per codeword: entry e holds the 8
   // copies of codebook 0, then the 8 of codebook 1 (256 bytes, every 16-byte
@@ -414,13 +457,7 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
   // instruction, so the 16 lanes of one LDS pass read 16 different bank
   // groups; each row still gets both codebooks over the pair of MFMAs.
   constexpr bool kPairCb = COPIES == 8 && M == 2;
-  if (tid < M * 256) {
-#pragma unroll
-    for (int k = 0; k < COPIES; ++k) {
-      const int c = (k + lane) % COPIES;
-      cb_lds[kPairCb ? (tid & 255) * 16 + (tid >> 8) * 8 + c : tid * COPIES + c] = cbv;
-    }
-  }
+  if constexpr (!STEP) stage_cb();
 #pragma unroll
   for (int i = 0; i < C::kXL; ++i) {
     const int grp = tid + i * kThreads;
@@ -553,8 +590,19 @@ __global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
     float s = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) s += part[(rb * kWaves + w) * 16 + rr];
-    bt.p[p].y[row0 + tid] = f2h(h2f(sc) * s);
+    const uint16_t out = f2h(h2f(sc) * s);
+    if constexpr (STEP)
+      __hip_atomic_store(bt.p[p].y + row0 + tid, out, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    else
+      bt.p[p].y[row0 + tid] = out;
   }
+  return true;
+}
+
+
+template <int M, int COPIES, int RB, int D, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_gemv_ks(const GemvBatch bt) {
+  ks_body<M, COPIES, RB, D, VEC, false>(bt, (int)blockIdx.x, [] { return true; });
 }
 
 // 1x16 with the codebook in LDS, one 128 KiB chunk (8192 codewords) at a
@@ -910,6 +958,119 @@ hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStrea
   return hipErrorInvalidValue;
 }
 
+// ---------------------------------------------------------------- decode step
+//
+// k_gemv_step runs a list of levels (each a grouped 2x8 product, as one
+// k_gemv_ks launch would) on a resident grid of one workgroup per CU.
+// Level l + 1 may read what level l wrote, so a workgroup reads level l + 1's
+// x only after every workgroup has finished level l: a counter that each
+// workgroup bumps after its last product of a level (its y stores completed
+// first), polled by one thread.  Everything a product reads apart from x is
+// loaded before that wait, so a workgroup that finishes a level early streams
+// the next level's first codes while the slowest ones finish.
+//
+// Every wait is bounded: after `spin` polls it sets the error flag and the
+// workgroup stops; a workgroup that sees the flag stops too, so the grid
+// always drains.  The last workgroup to leave resets the counters.
+
+// (M = 2, 8-bit codes, 16-byte code rows) body instantiations: (id, copies,
+// row blocks, ring depth)
+#define AQLM_STEP_VARIANTS(X)                                                                    \
+  X(0, 16, 1, 1) X(1, 16, 1, 2) X(2, 16, 1, 4) X(3, 16, 1, 8) X(4, 16, 2, 2) X(5, 16, 2, 4)       \
+  X(6, 16, 3, 2) X(7, 16, 4, 1) X(8, 16, 4, 2) X(9, 16, 5, 1) X(10, 16, 6, 1) X(11, 16, 7, 1)     \
+  X(12, 8, 1, 1) X(13, 8, 1, 2) X(14, 8, 1, 4) X(15, 8, 1, 8) X(16, 8, 2, 2) X(17, 8, 2, 4)
+
+int step_variant(int M, int copies, int rb, int d, bool vec) {
+  if (M != 2 || !vec) return -1;
+#define AQLM_STEP_FIND(ID, C, R, D) \
+  if (copies == C && rb == R && d == D) return ID;
+  AQLM_STEP_VARIANTS(AQLM_STEP_FIND)
+#undef AQLM_STEP_FIND
+  return -1;
+}
+
+// Thread 0 polls until `target` level signals have arrived; the verdict is
+// shared through LDS.  False: timed out here or elsewhere (error flag).
+// sync words: [0] level signals, [1] error flag, [2] workgroups that left;
+// one 64-bit load reads the counter and the flag together.
+__device__ bool step_wait(uint32_t* sync, uint32_t target, uint32_t spin, uint32_t* verdict) {
+  if (threadIdx.x == 0) {
+    uint32_t ok = 0;
+    for (uint32_t it = 0;; ++it) {
+      const uint64_t w =
+          __hip_atomic_load(reinterpret_cast<uint64_t*>(sync), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      // (the flag first: once any wait has given up, no workgroup starts
+      // another level)
+      if ((uint32_t)(w >> 32) != 0) break;
+      if ((uint32_t)w >= target) {
+        ok = 1;
+        break;
+      }
+      if (it >= spin) {
+        __hip_atomic_store(sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        break;
+      }
+    }
+    *verdict = ok;
+  }
+  __syncthreads();
+  const bool ok = *verdict != 0;
+  __syncthreads();
+  return ok;
+}
+
+// This workgroup is done with the level: its y stores have completed (they
+// are system-scope, written through to memory) before the counter moves.
+__device__ void step_signal(uint32_t* sync) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(sync, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// (The wait verdict lives in dynamic LDS right after the largest level's
+// region: a static __shared__ variable next to the dynamic array lost the
+// last word of the partial sums.)
+__global__ __launch_bounds__(kThreads) void k_gemv_step(const StepLevel* __restrict__ levels, int32_t nlev,
+                                                        uint32_t* sync, uint32_t spin, int32_t lds_bytes) {
+  extern __shared__ uint4 lds_all[];
+  uint32_t& verdict = *reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(lds_all) + lds_bytes);
+  const int nwg = (int)gridDim.x;
+  bool ok = true;
+  for (int l = 0; l < nlev && ok; ++l) {
+    const StepLevel& L = levels[l];
+    bool waited = l == 0;
+    // every workgroup waits for level l - 1 before it signals level l, so
+    // the counter reaches (l + 1) * nwg only once all have finished level l
+    auto wait = [&]() -> bool {
+      if (waited) return true;
+      waited = true;
+      return step_wait(sync, (uint32_t)l * (uint32_t)nwg, spin, &verdict);
+    };
+    const int variant = L.variant;
+    const int total = L.bt.total_wgs;
+    for (int v = (int)blockIdx.x; ok && v < total; v += nwg) {
+      switch (variant) {
+#define AQLM_STEP_CASE(ID, C, R, D) \
+  case ID: ok = ks_body<2, C, R, D, true, true>(L.bt, v, wait); break;
+        AQLM_STEP_VARIANTS(AQLM_STEP_CASE)
+#undef AQLM_STEP_CASE
+      }
+    }
+    if (ok) ok = wait();
+    if (ok) step_signal(sync);
+  }
+  // leave: the last workgroup out resets the counters (every other one has
+  // stopped reading them)
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint32_t out = __hip_atomic_fetch_add(sync + 2, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (out == (uint32_t)nwg - 1u) {
+      __hip_atomic_store(sync, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(sync + 2, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+  }
+}
+
 }  // namespace
 
 bool gemv_mfma_supported(int M, int B) {
@@ -935,8 +1096,23 @@ bool gemv_mfma_fits(const Layer* Ls, int count) {
 // Deal workgroups to problems, pick rows per workgroup and items per wave,
 // size LDS, and launch.  All problems share (M, B) and the code-pitch
 // alignment class.
-hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
-                            hipStream_t s) {
+// Ring depth k_gemv_ks runs for RB row blocks and nks K-slices per wave
+// (launch_ks_d's choice).
+int ks_ring_depth(int rb, int nks) {
+  const int dmax = rb >= 5 ? 1 : (rb >= 3 ? 2 : (rb == 2 ? 4 : 8));
+  const int dmin = (rb == 2 || rb == 3) ? 2 : 1;
+  if (dmax >= 8 && nks >= 8) return 8;
+  if (dmax >= 4 && nks >= 4) return 4;
+  if (dmax >= 2 && (nks >= 2 || dmin == 2)) return 2;
+  return dmin;
+}
+
+// Plans (and, without `plan`, launches) a grouped product.  With `plan` (the
+// decode-step planner, 2x8 only) nothing is launched: the workgroup split and
+// the k_gemv_ks variant are recorded, with row blocks per workgroup capped at
+// rb_cap_max (when > 0) and LDS at lds_limit.
+hipError_t gemv_mfma_impl(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
+                          hipStream_t s, StepLevel* plan, int rb_cap_max, size_t lds_limit) {
   if (count < 1 || count > kMaxProblems) return hipErrorInvalidValue;
   const int M = Ls[0].M, B = Ls[0].B;
   const bool packed = Ls[0].packed;
@@ -1011,7 +1187,8 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
     // At most rb_cap row blocks per workgroup (accumulator registers and
     // partial-sum space).  Larger layers run `rounds` workgroups per CU,
     // split evenly rather than leaving a short last round.
-    const int rb_cap = (B > 8) ? (cb_nks > 0 ? cb_rb_cap(cb_nks) : kMaxRB) : ks_rb_cap(M);
+    int rb_cap = (B > 8) ? (cb_nks > 0 ? cb_rb_cap(cb_nks) : kMaxRB) : ks_rb_cap(M);
+    if (rb_cap_max > 0 && rb_cap > rb_cap_max) rb_cap = rb_cap_max;
     const int blocks = (L.d_out + 15) / 16;
     const int rounds = (blocks + rb_cap * want - 1) / (rb_cap * want);
     const int rows_per_wg = (L.d_out + want * rounds - 1) / (want * rounds);
@@ -1043,7 +1220,8 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   const int xl = (B == 8) ? 4 : 8;
   if (xg_max > xl * kThreads) return hipErrorInvalidValue;
   const size_t base = (size_t)xg_max * 16 + (size_t)rb_max * kWaves * 16 * 4;
-  const size_t limit = 160 * 1024;
+  const size_t limit = lds_limit;
+  if (plan && B != 8) return hipErrorInvalidValue;
   if (B > 8 && cb_nks > 0) {
     if (packed) return launch_cb_shape<15, true>(bt, cb_nks, rb_max, s);
     return B == 15 ? launch_cb_shape<15>(bt, cb_nks, rb_max, s) : launch_cb_shape<16>(bt, cb_nks, rb_max, s);
@@ -1086,6 +1264,12 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   while (copies > 1 && base + per_copy * copies > limit) copies /= 2;
   if (base + per_copy * copies > limit) return hipErrorInvalidValue;
   const size_t lds = base + per_copy * copies;
+  if (plan) {
+    plan->bt = bt;
+    plan->variant = step_variant(M, copies, rb_max, ks_ring_depth(rb_max, nks_min), vec);
+    plan->lds_bytes = (int32_t)lds;
+    return plan->variant < 0 ? hipErrorInvalidValue : hipSuccess;
+  }
 #define AQLM_GEMV_COPIES(MM)                                                                     \
   switch (copies) {                                                                              \
     case 16: return vec ? launch_ks_rb<MM, 16, true>(bt, rb_max, nks_min, lds, s)                        \
@@ -1103,6 +1287,26 @@ hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t
   }
 #undef AQLM_GEMV_COPIES
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
+                            hipStream_t s) {
+  return gemv_mfma_impl(Ls, xs, ys, count, s, nullptr, 0, 160 * 1024);
+}
+
+hipError_t launch_step(const StepLevel* levels, int32_t nlev, int32_t grid, size_t lds, uint32_t* sync,
+                       uint32_t spin, hipStream_t s) {
+  if (nlev < 1 || grid < 1 || lds > kStepLdsLimit) return hipErrorInvalidValue;
+  {
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(k_gemv_step), (int)kStepLdsLimit);
+    if (e != hipSuccess) return e;
+  }
+  // cooperative: the runtime refuses the launch unless every workgroup can
+  // be resident at once, which the level barrier needs
+  int32_t lds_bytes = (int32_t)lds;
+  void* args[] = {(void*)&levels, (void*)&nlev, (void*)&sync, (void*)&spin, (void*)&lds_bytes};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(k_gemv_step), dim3(grid), dim3(kThreads), args,
+                                    (unsigned)lds + 16u, s);
 }
 
 }  // namespace aqlm

@@ -63,6 +63,32 @@ struct GemvBatch {
   int32_t xg_max;  // x groups staged in LDS by the largest problem
 };
 
+// Decode step (a persistent launch over many grouped 2x8 products): one
+// record per level, after a StepHeader, in device memory.
+struct StepLevel {
+  GemvBatch bt;
+  int32_t variant;    // k_gemv_ks body instantiation (an index into the step kernel's table)
+  int32_t lds_bytes;  // dynamic LDS this level needs
+};
+struct StepHeader {
+  uint32_t magic;
+  int32_t levels;
+  int32_t lds_bytes;  // maximum over the levels
+  int32_t grid;       // workgroups of the resident grid (CU count at planning time)
+};
+constexpr uint32_t kStepMagic = 0x50455453u;
+// Plans one level (no launch); rb_cap_max > 0 caps the row blocks per
+// workgroup, lds_limit the dynamic LDS.
+hipError_t gemv_mfma_impl(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
+                          hipStream_t s, StepLevel* plan, int rb_cap_max, size_t lds_limit);
+// LDS the step kernel leaves to the levels (it keeps a word of its own).
+constexpr size_t kStepLdsLimit = 160 * 1024 - 256;
+// sync: 3 words (level counter, error flag, exit counter), zero before the
+// first launch and left zero by a launch that completes (the error flag
+// stays set after a timed-out wait).
+hipError_t launch_step(const StepLevel* levels, int32_t nlev, int32_t grid, size_t lds, uint32_t* sync,
+                       uint32_t spin, hipStream_t s);
+
 hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s);
 bool gemv_mfma_supported(int M, int B);
 bool gemv_mfma_fits(const Layer* Ls, int count);

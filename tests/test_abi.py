@@ -2,6 +2,7 @@
 include/aqlm.h declares, and rejects bad arguments before touching the GPU
 (argument validation dereferences nothing, so fake pointers suffice)."""
 import ctypes
+import struct
 import os
 import re
 
@@ -268,3 +269,58 @@ def test_binding_checks_packed_shapes():
     words = torch.zeros((4, 3), dtype=torch.int32)
     with pytest.raises(ValueError):
         aq.packed_layer_args(words, cb, sc, 32)  # CPU tensors
+
+
+def _step_problems(n, d_out=64, d_in=1024):
+    Prob = _lib.GemvProblem
+    return (Prob * n)(*[Prob(P, P, P, P, P, d_out, d_in) for _ in range(n)])
+
+
+def test_decode_step_plan_on_the_host(lib):
+    """A plan is built on the host without touching the GPU (the pointers are
+    only recorded): header fields, size, and the refusals."""
+    one = lib.aqlm_gemv_step_plan_bytes(1)
+    assert one > 16 and lib.aqlm_gemv_step_plan_bytes(3) == 16 + 3 * (one - 16)
+    assert lib.aqlm_gemv_step_plan_bytes(0) == 0
+    sizes = (ctypes.c_int32 * 3)(3, 1, 2)
+    probs = _step_problems(6)
+    nbytes = lib.aqlm_gemv_step_plan_bytes(3)
+    buf = ctypes.create_string_buffer(nbytes)
+    assert lib.aqlm_gemv_step_plan(probs, sizes, 3, 2, 8, 8, ctypes.addressof(buf), nbytes) == OK
+    magic, levels, lds, grid = struct.unpack_from("<Iiii", buf.raw)
+    assert magic != 0 and levels == 3 and 0 < lds <= 160 * 1024 and grid > 0
+    assert lib.aqlm_gemv_step_plan(probs, sizes, 3, 2, 8, 8, ctypes.addressof(buf), nbytes - 1) == WORKSPACE
+    assert lib.aqlm_gemv_step_plan(None, sizes, 3, 2, 8, 8, ctypes.addressof(buf), nbytes) == NULL
+    assert lib.aqlm_gemv_step_plan(probs, sizes, 0, 2, 8, 8, ctypes.addressof(buf), nbytes) == SHAPE
+    bad = (ctypes.c_int32 * 3)(3, 0, 3)
+    assert lib.aqlm_gemv_step_plan(probs, bad, 3, 2, 8, 8, ctypes.addressof(buf), nbytes) == SHAPE
+    nine = (ctypes.c_int32 * 1)(9)
+    assert lib.aqlm_gemv_step_plan(_step_problems(9), nine, 1, 2, 8, 8, ctypes.addressof(buf), nbytes) == SHAPE
+    one_level = (ctypes.c_int32 * 1)(1)
+    for M, B in ((4, 8), (1, 8), (1, 16), (2, 12)):
+        assert lib.aqlm_gemv_step_plan(probs, one_level, 1, M, B, 8, ctypes.addressof(buf), nbytes) == UNSUP
+    # code rows that are not a multiple of 16 bytes, and x beyond the staging
+    assert lib.aqlm_gemv_step_plan(_step_problems(1, d_in=1032), one_level, 1, 2, 8, 8, ctypes.addressof(buf),
+                                   nbytes) == UNSUP
+    assert lib.aqlm_gemv_step_plan(_step_problems(1, d_in=65536), one_level, 1, 2, 8, 8, ctypes.addressof(buf),
+                                   nbytes) == UNSUP
+    assert lib.aqlm_gemv_step_plan(_step_problems(1, d_out=0), one_level, 1, 2, 8, 8, ctypes.addressof(buf),
+                                   nbytes) == SHAPE
+
+
+def test_decode_step_launch_refusals(lib):
+    """Checks that return before anything is launched (never a valid plan
+    with fake pointers: that one would launch)."""
+    nbytes = lib.aqlm_gemv_step_plan_bytes(1)
+    buf = ctypes.create_string_buffer(nbytes)
+    one_level = (ctypes.c_int32 * 1)(1)
+    assert lib.aqlm_gemv_step_plan(_step_problems(1), one_level, 1, 2, 8, 8, ctypes.addressof(buf), nbytes) == OK
+    assert lib.aqlm_gemv_step(None, P, P, 0, None) == NULL
+    assert lib.aqlm_gemv_step(ctypes.addressof(buf), None, P, 0, None) == NULL
+    assert lib.aqlm_gemv_step(ctypes.addressof(buf), P, None, 0, None) == NULL
+    assert lib.aqlm_gemv_step(ctypes.addressof(buf), P + 8, P, 0, None) == ALIGN
+    assert lib.aqlm_gemv_step(ctypes.addressof(buf), P, P + 4, 0, None) == ALIGN
+    junk = ctypes.create_string_buffer(nbytes)
+    assert lib.aqlm_gemv_step(ctypes.addressof(junk), P, P, 0, None) == SHAPE
+    assert lib.aqlm_gemv_step_status(None, None) == NULL
+    assert lib.aqlm_gemv_step_status(P + 4, None) == ALIGN

@@ -1030,3 +1030,179 @@ def test_packed_codes_refused_where_unsupported():
         aq().gemv(words, cb, sc, x[0], out=y)
     torch.cuda.synchronize()
     assert not y.any()
+
+
+# ------------------------------------------- decode step (one persistent launch)
+
+def _step_layer(seed, d_out, d_in, x=None):
+    """A 2x8 layer on the GPU with its host copy; x: a GPU fp16 vector to
+    read instead of the layer's own (an earlier level's output)."""
+    lay = synth.layer(seed, d_out, d_in, 2, 8)
+    codes, cb, sc, xd = to_device(lay)
+    y = torch.full((d_out,), float("nan"), dtype=torch.float16, device="cuda")
+    return lay, (codes, cb, sc, xd[0] if x is None else x, y)
+
+
+def _grouped_reference(levels):
+    """The same levels as separate grouped launches, one per level, into
+    fresh outputs (kernel boundaries order them)."""
+    outs = []
+    for lv in levels:
+        ys = [torch.full_like(p[4], float("nan")) for p in lv]
+        aq().gemv_grouped([(p[0], p[1], p[2], p[3], y) for p, y in zip(lv, ys)])
+        outs.append(ys)
+    torch.cuda.synchronize()
+    return outs
+
+
+def test_decode_step_chained_levels_match_oracle():
+    """Level 1 reads level 0's output and level 2 level 1's: the step must
+    order the levels across the whole grid.  Each output is checked against
+    the oracle run through the same chain (its own fp16-rounded outputs as the
+    next inputs), within the elementwise bound plus the effect of the
+    previous level's bound through |W|; and bit for bit against the same
+    levels launched one by one with aqlm_gemv_grouped."""
+    print("[step] chained levels", flush=True)
+    lay0, p0 = _step_layer(21_000, 4096, 4096)
+    lay1, p1 = _step_layer(21_001, 2048, 4096, x=p0[4])
+    lay2, p2 = _step_layer(21_002, 1024, 4096, x=p0[4])
+    lay3, p3 = _step_layer(21_003, 4096, 2048, x=p1[4])
+    levels = [[p0], [p1, p2], [p3]]
+    step = aq().DecodeStep(levels)
+    step.run()
+    step.status()
+    # oracle chain: x of a level = the oracle's fp16-rounded output of the previous one
+    def run_oracle(lay, x_f16, err_in):
+        w = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+        ref = oracle.matmul_f16(w, x_f16[None, :])[0]
+        absw = abs_codeword_sums(lay)
+        bound = elementwise_bound(w, x_f16[None, :], ref[None, :], absw)[0]
+        if err_in is not None:
+            bound = bound * 1.01 + np.abs(w.view(np.float16).astype(np.float64)) @ err_in
+        return ref, bound
+    ref0, b0 = run_oracle(lay0, lay0.x[0], None)
+    x1 = ref0.astype(np.float16)
+    e0 = b0 + np.abs(ref0 - x1.astype(np.float64))
+    ref1, b1 = run_oracle(lay1, x1, e0)
+    ref2, b2 = run_oracle(lay2, x1, e0)
+    x3 = ref1.astype(np.float16)
+    e1 = b1 + np.abs(ref1 - x3.astype(np.float64))
+    ref3, b3 = run_oracle(lay3, x3, e1)
+    for name, (p, ref, bound) in {"l0": (p0, ref0, b0), "l1a": (p1, ref1, b1), "l1b": (p2, ref2, b2),
+                                  "l2": (p3, ref3, b3)}.items():
+        got = fp16_to_np(p[4]).astype(np.float64)
+        assert np.all(np.isfinite(got)), name
+        assert rel_l2(got, ref) <= TOL, (name, rel_l2(got, ref))
+        worst = int(np.argmax(np.abs(got - ref) - bound))
+        assert np.all(np.abs(got - ref) <= bound), (name, worst, abs(got[worst] - ref[worst]), bound[worst])
+    # the same chain, one grouped launch per level (level l's y feeds level l + 1)
+    y0 = torch.empty_like(p0[4])
+    y1 = torch.empty_like(p1[4])
+    y2 = torch.empty_like(p2[4])
+    y3 = torch.empty_like(p3[4])
+    aq().gemv_grouped([(p0[0], p0[1], p0[2], p0[3], y0)])
+    aq().gemv_grouped([(p1[0], p1[1], p1[2], y0, y1), (p2[0], p2[1], p2[2], y0, y2)])
+    aq().gemv_grouped([(p3[0], p3[1], p3[2], y1, y3)])
+    torch.cuda.synchronize()
+    for a, b in ((p0[4], y0), (p1[4], y1), (p2[4], y2), (p3[4], y3)):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def _block_levels(seed, shapes, blocks):
+    """Decode-step levels of `blocks` transformer blocks with the given
+    projection shapes (q, k, v, o, gate, up, down), independent inputs:
+    grouped q/k/v, o, grouped gate/up, down."""
+    levels, lays = [], []
+    for b in range(blocks):
+        made = [_step_layer(seed + 16 * b + i, o, i_) for i, (o, i_) in enumerate(shapes)]
+        lays += [m[0] for m in made]
+        ps = [m[1] for m in made]
+        x_attn, x_mlp = ps[0][3], ps[4][3]
+        ps = [(c, cb, s, x_attn if i in (1, 2) else (x_mlp if i == 5 else x), y)
+              for i, (c, cb, s, x, y) in enumerate(ps)]
+        levels += [[ps[0], ps[1], ps[2]], [ps[3]], [ps[4], ps[5]], [ps[6]]]
+    return levels, lays
+
+
+def test_decode_step_7b_blocks_match_grouped_launches_and_oracle():
+    """Two Llama-2-7B blocks (8 levels) in one launch: every output bit for
+    bit the grouped launches' (same work split, same arithmetic), and
+    sampled rows of each against the oracle."""
+    print("[step] 7B blocks", flush=True)
+    shapes = [(4096, 4096)] * 4 + [(11008, 4096)] * 2 + [(4096, 11008)]
+    levels, lays = _block_levels(22_000, shapes, 2)
+    step = aq().DecodeStep(levels)
+    step.run()
+    step.status()
+    ref = _grouped_reference(levels)
+    flat = [p for lv in levels for p in lv]
+    flat_ref = [y for ys in ref for y in ys]
+    for p, y in zip(flat, flat_ref):
+        assert torch.equal(p[4].view(torch.int16), y.view(torch.int16))
+    # lays are in shape order per block; the problems in level order are
+    # q, k, v, o, gate, up, down as well
+    rows = np.array([0, 1, 15, 16, 1000, 2047, 4095])
+    for lay, p in zip(lays, flat):
+        r = rows[rows < lay.d_out]
+        x = p[3].cpu().numpy().view(np.uint16)[None, :]
+        w = oracle.dequantize_rows(lay.codes, lay.codebooks, lay.scales, r)
+        want = oracle.matmul_f16(w, x)
+        got = fp16_to_np(p[4])[None, r].astype(np.float64)
+        bound = elementwise_bound(w, x, want, abs_codeword_sums(lay, r))
+        assert np.all(np.abs(got - want) <= bound)
+
+
+def test_decode_step_reruns_are_identical():
+    """The counters are left zero by each launch: five runs in a row, each
+    status clean, all outputs identical."""
+    levels, _ = _block_levels(23_000, [(1024, 1024)] * 4 + [(2816, 1024)] * 2 + [(1024, 2816)], 3)
+    step = aq().DecodeStep(levels)
+    outs = []
+    for _ in range(5):
+        for lv in levels:
+            for p in lv:
+                p[4].fill_(float("nan"))
+        step.run()
+        step.status()
+        outs.append([p[4].clone() for lv in levels for p in lv])
+    for o in outs[1:]:
+        assert all(torch.equal(a.view(torch.int16), b.view(torch.int16)) for a, b in zip(outs[0], o))
+    assert int(step.sync[0]) == 0 and int(step.sync[2]) == 0
+
+
+def test_decode_step_barrier_timeout_is_reported_and_recovers():
+    """A bounded wait that gives up: level 0 pairs a large layer with a
+    16-row one, so the workgroup of the small one reaches level 1's barrier
+    long before the others finish; with one poll allowed it times out.  The
+    flag is reported (AQLM_ERR_TIMEOUT), level 1 is left unwritten, the
+    launch ends normally, and the next run with the default limit computes
+    everything."""
+    print("[step] timeout", flush=True)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(24_000)
+    big = synth.device_layer(24_001, 28672, 8192, 2, 8)
+    small = synth.device_layer(24_002, 16, 8192, 2, 8)
+    nxt = synth.device_layer(24_003, 4096, 4096, 2, 8)
+    ys = [torch.full((d,), float("nan"), dtype=torch.float16, device="cuda") for d in (28672, 16, 4096)]
+    levels = [[(big[0], big[1], big[2], big[3][0], ys[0]), (small[0], small[1], small[2], small[3][0], ys[1])],
+              [(nxt[0], nxt[1], nxt[2], nxt[3][0], ys[2])]]
+    step = aq().DecodeStep(levels)
+    step.run(spin_limit=1)
+    with pytest.raises(aq().AqlmError) as e:
+        step.status()
+    assert e.value.status == 8
+    assert torch.isnan(ys[2].float()).all()          # level 1 never ran
+    assert int(step.sync[0]) == 0 and int(step.sync[2]) == 0   # counters reset by the last workgroup out
+    step.run()
+    step.status()
+    ref = _grouped_reference(levels)
+    for got, want in zip(ys, [y for r in ref for y in r]):
+        assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+
+
+def test_decode_step_refuses_other_formats():
+    lay = synth.layer(25_000, 64, 1024, 4, 8)
+    codes, cb, sc, x = to_device(lay)
+    y = torch.empty(64, dtype=torch.float16, device="cuda")
+    with pytest.raises(aq().AqlmError):
+        aq().DecodeStep([[(codes, cb, sc, x[0], y)]])
