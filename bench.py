@@ -432,7 +432,8 @@ def batch_rows(aq, torch, cases=None):
     dequantization)."""
     rows = []
     for M, B in ((1, 16), (4, 8), (2, 12), (2, 16)):
-        for n in (1, 4, 16, 256, 2048):
+        ns = (1, 4, 16, 256, 2048) if cases is None else sorted({c[2] for c in cases if c[:2] == (M, B)})
+        for n in ns:
             from paper_2401_06118_amd import format as fmt
             shp = fmt.AqlmShape(11008, 4096, M, B)
             name = f"11008x4096 {M}x{B}"

@@ -124,6 +124,10 @@ constexpr int64_t kChunkedMax = 64;
 // with the token count: chunks pay off up to two of them.
 constexpr int64_t kChunkedMax16 = 32;
 
+// Rows from which two wide codebooks take the prefill kernel.
+constexpr int64_t kPrefillMin2x12 = 192;
+constexpr int64_t kPrefillMin2xWide = 96;
+
 // From this many tokens aqlm_gemm dequantizes the whole matrix into the
 // caller's workspace once and runs the dense product (when d_in allows it).
 constexpr int64_t kTwoPassMin = 64;
@@ -202,8 +206,14 @@ int gemm_dispatch(const aqlm::Layer& L, int64_t n, const uint16_t* x, uint16_t* 
     }
     return AQLM_OK;
   }
-  // More tokens: dequantized weight tiles feed a dense MFMA product.
-  if (n > kSmallBatchMax && aqlm::prefill_supported(L)) return status_of(aqlm::launch_prefill(L, (int32_t)n, x, y, s));
+  // More tokens: dequantized weight tiles feed a dense MFMA product.  Two
+  // wide codebooks gather every codeword from L2 there, which pays off only
+  // from more rows (11008 x 4096, tiled kernel vs prefill: 2x12 92 vs 134 us
+  // at 128 rows, 163 vs 147 at 256, 965 vs 551 at 2048; 2x16 140 vs 153 at
+  // 64, 163 vs 154 at 128, 1605 vs 623 at 2048).
+  const int64_t prefill_min = (L.M == 2 && L.B > 8) ? (L.B == 12 ? kPrefillMin2x12 : kPrefillMin2xWide) : 0;
+  if (n > kSmallBatchMax && n >= prefill_min && aqlm::prefill_supported(L))
+    return status_of(aqlm::launch_prefill(L, (int32_t)n, x, y, s));
   if (aqlm::mfma_supported(L)) return status_of(aqlm::launch_gemm_mfma(L, (int32_t)n, x, y, s));
   // Formats the matrix-core kernel does not tile (M = 3, 5, 6, 7): one
   // matrix-vector launch per activation row.

@@ -15,7 +15,8 @@
 // (producers) fill the next K-step's tiles while the consumers multiply the
 // current ones: a K-step is 64 inputs (8 groups); per step the producers
 // dequantize 128 rows x 8 groups of weights (codeword lookups from LDS
-// codebook copies for 8-bit codes, 16-byte L2 gathers for 16-bit codes) and
+// codebook copies for 8-bit codes, 16-byte L2 gathers for wider codes, one
+// or two codebooks) and
 // copy BN tokens x 64 inputs of x.  Both tiles are double-buffered in LDS
 // with a row pitch of 9 x 16 bytes, so the fragment reads of 16 consecutive
 // rows hit 16 different bank quads.  Producer global loads run two K-steps
@@ -184,13 +185,14 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
         xv[s][i] = a.x[(size_t)tc * G + gxc];
       }
     };
-    // 16-bit codes: the codewords of step k come from L2 with 16-byte
-    // gathers, issued a step before they are stored.
-    uint4 gcw[2][4];
+    // Wide codes: the codewords of step k come from L2 with 16-byte
+    // gathers (codebook m's entries start 2^B codewords after codebook
+    // m - 1's), issued a step before they are stored.
+    uint4 gcw[2][4 * M];
     auto p_gather = [&](auto set) {
       constexpr int s = decltype(set)::value;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gcw[s][q] = a.cb[code_at<B>(cw[s], q)];
+      for (int q = 0; q < 4 * M; ++q) gcw[s][q] = a.cb[((uint32_t)(q % M) << B) + code_at<B>(cw[s], q)];
     };
     // Dequantize this thread's 4 groups of K-step k (register set s) and
     // store them and its x token row into LDS buffer k % 2.
@@ -209,7 +211,7 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
             const uint32_t addr = ((uint32_t)(m * 256) + code) * (uint32_t)(P::kCopies * 16) + copy_off;
             cwv[m] = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(cb_lds) + addr);
           } else {
-            cwv[m] = gcw[s][q];  // gathered one step earlier
+            cwv[m] = gcw[s][q * M + m];  // gathered one step earlier
           }
         }
         // Sum of the M codewords in fp32, ascending m, rounded once to fp16
@@ -375,11 +377,19 @@ hipError_t run_prefill(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y
 }  // namespace
 
 bool prefill_supported(const Layer& L) {
-  if (L.B > 8) return L.M == 1;
+  if (L.B > 8) return L.M == 1 || L.M == 2;
   return L.M == 1 || L.M == 2 || L.M == 4;
 }
 
 hipError_t launch_prefill(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s) {
+  if (L.B > 8 && L.M == 2) {
+    switch (L.B) {
+      case 12: return run_prefill<2, 12>(L, n, x, y, s);
+      case 15: return run_prefill<2, 15>(L, n, x, y, s);
+      case 16: return run_prefill<2, 16>(L, n, x, y, s);
+    }
+    return hipErrorInvalidValue;
+  }
   if (L.B == 16) return L.M == 1 ? run_prefill<1, 16>(L, n, x, y, s) : hipErrorInvalidValue;
   if (L.B == 15) return L.M == 1 ? run_prefill<1, 15>(L, n, x, y, s) : hipErrorInvalidValue;
   switch (L.M) {

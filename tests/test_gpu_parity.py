@@ -895,10 +895,12 @@ def test_2x12_dequantize_special_values_bit_exact():
     assert_bits_equal(dequant_gpu(lay), oracle.dequantize(lay.codes, lay.codebooks, lay.scales))
 
 
-@pytest.mark.parametrize("B", [12, 16])
-@pytest.mark.parametrize("n", [4, 16, 32, 100, 300])
+@pytest.mark.parametrize("B", [12, 15, 16])
+@pytest.mark.parametrize("n", [4, 16, 32, 100, 200, 300])
 def test_2xwide_gemm_matches_oracle(B, n):
-    """Small batch (chunks of 16), the tiled kernel, and the workspace path."""
+    """Small batch (chunks of 16), the tiled kernel, the prefill kernel with
+    two codebooks gathered from L2 (from 96 rows, 192 for 2x12; ragged row
+    and token tiles) and the workspace path."""
     print(f"[2x{B} gemm] n={n}", flush=True)
     lay = synth.layer(17_900 + B + n, 1100, 2048, 2, B, n=n)
     codes, cb, sc, x = to_device(lay)
@@ -907,6 +909,19 @@ def test_2xwide_gemm_matches_oracle(B, n):
     torch.cuda.synchronize()
     check_products(lay, fp16_to_np(y1))
     check_products(lay, fp16_to_np(y2))
+
+
+@pytest.mark.parametrize("B", [12, 16])
+def test_2xwide_prefill_layer_sampled_rows(B):
+    """11008 x 4096 with 2048 rows through the prefill kernel (256-token
+    tiles, every XCD), rows sampled."""
+    print(f"[2x{B} prefill] n=2048", flush=True)
+    lay = synth.layer(18_100 + B, 11008, 4096, 2, B, n=2048)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemm_small_batch(codes, cb, sc, x)
+    torch.cuda.synchronize()
+    rows = np.array([0, 1, 127, 128, 5503, 11006, 11007] + list(range(300, 11008, 1499)))
+    check_products(lay, fp16_to_np(y), rows=rows)
 
 
 def test_2x12_high_code_bits_are_ignored():
