@@ -14,12 +14,12 @@ attention, norms, embeddings and the LM head are not part of the step).
 
 Also reported on the same JSON line:
   roofline      the dominant kernel against 8 TB/s: algorithmic bytes per
-                launch over its average launch duration.  The duration is
-                the one a committed rocprofv3 kernel trace of this command
-                records over the timed graph replays (profiles/
-                kernel_durations.txt, keyed by kernel source digest), or,
-                without one, the event-timed replay region divided by its
-                launches (launch gaps included); both are on the line.
+                launch over its average launch duration, measured live with
+                HIP events around the timed graph replays (gaps included);
+                beside it, the committed rocprofv3 kernel trace of this
+                command for the same kernel source (profiles/
+                kernel_durations.txt): its per-kernel average and the share
+                of its step the kernels filled.
                 ``traffic`` is the HBM bytes per launch from the committed
                 counter summary (null once the source has changed);
   cpu_baseline  the CPU oracle (dequantize + fp64 product) timed on the host
@@ -86,6 +86,8 @@ def parse_args():
                          "through both kernel families (codeword gathers, partial-product tables) and exit")
     ap.add_argument("--backward", action="store_true",
                     help="only time the gradients through Eq. 2 (aqlm_backward) and exit")
+    ap.add_argument("--persistent", action="store_true",
+                    help="only the workload's step as one persistent launch (aqlm_gemv_step) beside its graph")
     ap.add_argument("--single-layers", action="store_true",
                     help="only the single-layer matrix-vector rows (incl. bit-packed codes)")
     ap.add_argument("--beam-search", action="store_true",
@@ -272,11 +274,12 @@ def measured_traffic(kernel_key: str, digest: str):
 
 
 def traced_duration(kernel_key: str, digest: str):
-    """(average kernel duration in us, dispatches per step) over the timed
-    graph replays, from the committed rocprofv3 kernel-trace summary of this
-    workload, or None if there is none for this kernel source."""
+    """(average kernel duration in us, dispatches per step, the traced run's
+    event-timed ms per step) over the timed graph replays, from the committed
+    rocprofv3 kernel-trace summary of this workload, or None if there is none
+    for this kernel source."""
     f = _profile_lookup("kernel_durations.txt", kernel_key, digest)
-    return (float(f[0]), float(f[1])) if f else None
+    return (float(f[0]), float(f[1]), float(f[2])) if f else None
 
 
 def summarize_trace(csv_path: str):
@@ -605,8 +608,10 @@ def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False):
     """Build a decode step, capture it as one graph and time its replays."""
     layers = decode_step_layers(model, M, B, seed0)
     step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
+    log(f"{model} {M}x{B}: {len(layers)} layers built")
     launches = launches_by_dependency(layers, aq)
     graph = graph_of(launches)
+    log(f"{model} {M}x{B}: graph captured")
     ms = time_steps(graph.replay, steps, warmup, markers=markers)
     spread = step_spread(graph.replay, max(steps, 20))
     return layers, launches, graph, ms, spread, step_bytes
@@ -674,27 +679,39 @@ def main():
         return
 
     model, M, B = WORKLOADS[args.workload]
+    if args.persistent:
+        layers, launches, graph, ms, spread, step_bytes = decode_step(model, M, B, step_seed(M), aq, args.steps,
+                                                                      args.warmup)
+        row = persistent_step_row(layers, graph, aq, torch, args.steps, step_bytes, ms)
+        print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "persistent_step": row}), flush=True)
+        return
     layers, launches, graph, ms, spread, step_bytes = decode_step(
         model, M, B, step_seed(M), aq, args.steps, args.warmup, markers=True)
     log(f"{args.workload}: {len(layers)} layers in {len(launches)} launches, {step_bytes / 1e9:.3f} GB per step; "
         f"step {ms:.4f} ms (graph replay)")
 
     # Dominant kernel: every launch of the step is the matrix-vector kernel
-    # (grouped or single).  Its average launch duration comes from the
-    # committed kernel trace of this command when one exists for the current
-    # source; the event-timed replay region divided by its launches (which
-    # includes the gaps between launches) is reported beside it.
+    # (grouped or single).  Its average launch duration is measured live: HIP
+    # events on the launch stream around the timed graph replays, divided by
+    # the launches (gaps between kernels included).  The committed kernel
+    # trace of this command (same kernel source) is reported beside it: its
+    # per-kernel average, and what share of its own run's step the kernels
+    # filled, which bounds how much of the live figure is gaps.  Boxes differ
+    # by several per cent, so the two agree only when taken on the same box.
     bytes_per_launch = step_bytes / len(launches)
-    avg_events_us = ms * 1e3 / len(launches)
-    digest = source_digest("gemv_mfma.hip", "stream_common.h", "common.h")
+    avg_us = ms * 1e3 / len(launches)
+    digest = source_digest("gemv_mfma.hip", "stream_common.h", "common.h", "launch.h")
     kname = kernel_name(M, B)
     key = f"{kname}:{args.workload}"
     traced = traced_duration(key, digest)
+    trace = None
     if traced is not None:
-        avg_us, source = traced[0], ("rocprofv3 kernel trace of this command over the timed graph replays "
-                                     "(profiles/kernel_durations.txt, same kernel source)")
-    else:
-        avg_us, source = avg_events_us, "HIP events over the timed graph replays / launches (gaps included)"
+        trace = {"avg_launch_us": traced[0], "dispatches_per_step": traced[1],
+                 "kernel_ms_per_step": traced[0] * traced[1] / 1e3, "traced_run_ms_per_step": traced[2],
+                 "kernel_share_of_step": traced[0] * traced[1] / 1e3 / traced[2],
+                 "frac": bytes_per_launch / (traced[0] * 1e3) / HBM_PEAK_GBS,
+                 "source": "rocprofv3 kernel trace of this command over the timed graph replays "
+                           "(profiles/kernel_durations.txt)"}
     achieved = bytes_per_launch / (avg_us * 1e3)
     traffic = measured_traffic(key, digest)
 
@@ -733,10 +750,8 @@ def main():
             "traffic": traffic,
             "bytes_per_launch": bytes_per_launch,
             "avg_launch_us": avg_us,
-            "duration_source": source,
-            "avg_launch_us_events": avg_events_us,
-            "frac_events": bytes_per_launch / (avg_events_us * 1e3) / HBM_PEAK_GBS,
-            "traced_kernel_ms_per_step": traced[0] * traced[1] / 1e3 if traced else None,
+            "duration_source": "HIP events around the timed graph replays on the launch stream / launches",
+            "trace": trace,
             "source_digest": digest,
         },
     }
