@@ -119,11 +119,14 @@ def brute_force_dequant(codes, codebooks, scales):
 
 
 @pytest.mark.parametrize("M,B,g", [(1, 2, 8), (2, 2, 8), (3, 3, 4), (4, 4, 2), (2, 4, 8), (1, 4, 1),
-                                   (2, 12, 8), (2, 15, 8), (2, 16, 8)])
+                                   (2, 12, 8), (2, 15, 8), (2, 16, 8),
+                                   (4, 8, 16), (8, 8, 32), (15, 8, 64), (16, 4, 64)])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_dequant_matches_one_hot_brute_force(M, B, g, seed):
     """Includes two codebooks of 12-, 15- and 16-bit codes (the 3- and 4-bit
-    settings of App. "Experimental Configurations"), stored as uint16."""
+    settings of App. "Experimental Configurations"), stored as uint16, and
+    the larger groups of the codebooks-versus-groups ablation (4x8 with
+    groups of 16, 8x8 with 32, 15x8 with 64)."""
     rng = np.random.default_rng(100 * seed + 10 * M + B)
     d_out, groups = int(rng.integers(1, 9)), int(rng.integers(1, 5))
     codebooks = rng.standard_normal((M, 1 << B, g)).astype(np.float16)
@@ -550,3 +553,25 @@ def test_packed_dequantize_matches_unpacked():
     packed = fmt.pack_codes(lay.codes, 12)
     assert np.array_equal(oracle.dequantize_packed(packed, lay.codebooks, lay.scales, 96, 12),
                           oracle.dequantize(lay.codes, lay.codebooks, lay.scales))
+
+
+@pytest.mark.parametrize("M,g", [(4, 16), (8, 32), (15, 64)])
+def test_large_groups_unit_vector_codebooks_closed_form(M, g):
+    """Codeword e of every codebook is the unit vector e_(e mod g) (as fp16):
+    group j of row i is the sum over m of unit vectors, so with unit scales
+    y_i = sum_j sum_m x[g j + (b_ijm mod g)] exactly (fp64, small integers
+    in x).  Pins the group-size indexing of codes, codewords and inputs."""
+    rng = np.random.default_rng(500 + g)
+    d_out, groups = 5, 3
+    d_in = groups * g
+    cb = np.zeros((M, 256, g), dtype=np.float16)
+    for e in range(256):
+        cb[:, e, e % g] = 1.0
+    codes = rng.integers(0, 256, size=(d_out, groups, M), dtype=np.uint8)
+    scales = np.ones(d_out, dtype=np.float16)
+    x = rng.integers(-3, 4, size=(1, d_in)).astype(np.float16)
+    w = oracle.dequantize(codes, cb, scales, g)
+    y = oracle.matmul_f16(w, x)[0]
+    want = np.array([sum(float(x[0, g * j + (int(codes[i, j, m]) % g)]) for j in range(groups) for m in range(M))
+                     for i in range(d_out)])
+    assert np.array_equal(y, want)
