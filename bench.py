@@ -101,12 +101,12 @@ def parse_args():
 
 
 class DeviceLayer:
-    def __init__(self, seed, d_out, d_in, M, B, n=1, x=None, packed=False):
+    def __init__(self, seed, d_out, d_in, M, B, n=1, x=None, packed=False, g=8):
         from paper_2401_06118_amd import format as fmt
         from paper_2401_06118_amd import synth
-        self.shape = fmt.AqlmShape(d_out, d_in, M, B)
+        self.shape = fmt.AqlmShape(d_out, d_in, M, B, g)
         make = synth.device_packed_layer if packed else synth.device_layer
-        self.codes, self.codebooks, self.scales, xg = make(seed, d_out, d_in, M, B, n=n)
+        self.codes, self.codebooks, self.scales, xg = make(seed, d_out, d_in, M, B, g=g, n=n)
         self.x = xg if x is None else x
         import torch
         self.y = torch.empty((n, d_out), dtype=torch.float16, device="cuda")
@@ -405,13 +405,18 @@ def single_layer_rows(aq, torch):
         "11008x4096 2x15 packed": (11008, 4096, 2, 15),
         "11008x4096 1x15 packed": (11008, 4096, 1, 15),
         "4096x4096 2x12 packed": (4096, 4096, 2, 12),
+        # larger groups (about two bits per weight, like 2x8)
+        "4096x4096 4x8 gs16": (4096, 4096, 4, 8),
+        "4096x4096 8x8 gs32": (4096, 4096, 8, 8),
+        "4096x4096 15x8 gs64": (4096, 4096, 15, 8),
     }.items():
         from paper_2401_06118_amd import format as fmt
         packed = name.endswith("packed")
-        shp = fmt.AqlmShape(d_out, d_in, M, B)
+        g = int(name.split(" gs")[1]) if " gs" in name else 8
+        shp = fmt.AqlmShape(d_out, d_in, M, B, g)
         code_bytes = shp.packed_codes_bytes() if packed else shp.codes_bytes()
         reps = max(2, min(256, (1 << 30) // code_bytes + 1))
-        layers = [DeviceLayer(900000 + i, d_out, d_in, M, B, packed=packed) for i in range(reps)]
+        layers = [DeviceLayer(900000 + i, d_out, d_in, M, B, packed=packed, g=g) for i in range(reps)]
         calls = [lambda L=L: L.gemv(aq) for L in layers]
         g = graph_of(calls)
         ms = time_steps(g.replay, steps=3, warmup=1) / reps

@@ -34,6 +34,13 @@
  *   B = 15 or 16, M = 1   one codebook of 32768 or 65536 entries (2 bits);
  *   B = 12, M = 2         two codebooks of 4096 entries (3 bits);
  *   B = 15 or 16, M = 2   two codebooks of 32768 or 65536 entries (4 bits).
+ * Larger groups (the codebooks-versus-groups settings of the ablation:
+ * 4x8 with groups of 16, 8x8 with 32, 15x8 with 64): g = 16, 32 or 64 with
+ * B = 8 and 1 <= M <= 16, codebooks [M][256][g].  aqlm_dequantize, aqlm_gemv,
+ * aqlm_gemv_grouped (gather path), aqlm_gemm_small_batch (one matrix-vector
+ * product per row), aqlm_gemm and aqlm_gemm_noalloc take them (for these the
+ * two-pass product has the same workspace rule); every other entry point
+ * returns AQLM_ERR_UNSUPPORTED.  Here d_out * d_in / 8 must stay below 2^31.
  * Codes wider than 8 bits are stored one per uint16 by default.  Bit-packed
  * codes (the storage the paper's bits-per-parameter figures count, Sec. 3.3):
  * pass B | AQLM_PACKED for B = 12 (M = 2) or 15 (M = 1 or 2).  Each row of

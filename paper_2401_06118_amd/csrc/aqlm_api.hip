@@ -10,6 +10,7 @@
 #include <tuple>
 
 #include "../../include/aqlm.h"
+#include "groups.h"
 #include "launch.h"
 
 namespace aqlm {
@@ -114,6 +115,31 @@ int check_layer(const void* codes, const uint16_t* codebooks, const uint16_t* sc
 
 int status_of(hipError_t e) { return e == hipSuccess ? AQLM_OK : AQLM_ERR_HIP; }
 
+// Groups of 16, 32 or 64 inputs (8-bit codes, up to 16 codebooks): validated
+// here and served by the group kernels (csrc/groups.hip).
+int check_group_layer(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                      int64_t d_in, int32_t M, int32_t B, int32_t g, aqlm::GroupLayer* L) {
+  if (!codes || !codebooks || !scales) return AQLM_ERR_NULL;
+  if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return AQLM_ERR_SHAPE;
+  if (!aqlm::groups_supported(M, B, g)) return AQLM_ERR_UNSUPPORTED;
+  // (8-input chunks of the whole matrix are counted in 32 bits)
+  if (d_out >= (int64_t(1) << 31) || d_in >= (int64_t(1) << 31) || d_out * (d_in / 8) >= (int64_t(1) << 31))
+    return AQLM_ERR_SHAPE;
+  if (!aligned(codes, 16) || !aligned(codebooks, 16) || !aligned(scales, 2)) return AQLM_ERR_ALIGN;
+  *L = aqlm::GroupLayer{static_cast<const uint8_t*>(codes), codebooks, scales, (int32_t)d_out, (int32_t)d_in, M, g};
+  return AQLM_OK;
+}
+
+// A validated layer of either kind: groups of 8 (every kernel) or larger
+// groups (the group kernels only).
+struct AnyLayer {
+  bool big = false;
+  aqlm::Layer L{};
+  aqlm::GroupLayer GL{};
+  int64_t d_out() const { return big ? GL.d_out : L.d_out; }
+  int64_t d_in() const { return big ? GL.d_in : L.d_in; }
+};
+
 // Above this many tokens the dequantize-then-multiply prefill kernel is used
 // (up to kChunkedMax tokens in chunks of kSmallBatchMax when the small-batch
 // kernel covers the format: its time barely grows up to 16 tokens, while the
@@ -160,27 +186,57 @@ hipError_t gemv_dispatch(const aqlm::Layer& L, const uint16_t* x, uint16_t* y, h
   return aqlm::launch_gemv(L, x, y, s);
 }
 
+
+int gemm_dispatch(const aqlm::Layer& L, int64_t n, const uint16_t* x, uint16_t* y, hipStream_t s);
+
+int check_any(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
+              int32_t M, int32_t B, int32_t g, AnyLayer* A, bool allow_packed = false) {
+  if (g != 8 && g > 0 && (B & AQLM_PACKED) == 0 && aqlm::groups_supported(M, B, g)) {
+    A->big = true;
+    return check_group_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &A->GL);
+  }
+  A->big = false;
+  return check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &A->L, allow_packed);
+}
+
+hipError_t any_dequant(const AnyLayer& A, uint16_t* w, hipStream_t s) {
+  return A.big ? aqlm::launch_dequant_groups(A.GL, w, s) : aqlm::launch_dequant(A.L, w, s);
+}
+
+// Workspace-free product of n rows: the group kernel once per row for large
+// groups (a format with no batched kernel), gemm_dispatch otherwise.
+int any_gemm_dispatch(const AnyLayer& A, int64_t n, const uint16_t* x, uint16_t* y, hipStream_t s) {
+  if (!A.big) return gemm_dispatch(A.L, n, x, y, s);
+  for (int64_t t = 0; t < n; ++t) {
+    const hipError_t e = aqlm::launch_gemv_groups(A.GL, x + t * A.GL.d_in, y + t * A.GL.d_out, s);
+    if (e != hipSuccess) return AQLM_ERR_HIP;
+  }
+  return AQLM_OK;
+}
+
 }  // namespace
 
 extern "C" {
 
 int aqlm_dequantize(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                     int64_t d_in, int32_t M, int32_t B, int32_t g, uint16_t* w_out, void* stream) {
-  aqlm::Layer L;
-  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L, true);
+  AnyLayer A;
+  const int st = check_any(codes, codebooks, scales, d_out, d_in, M, B, g, &A, true);
   if (st != AQLM_OK) return st;
   if (!w_out) return AQLM_ERR_NULL;
   if (!aligned(w_out, 16)) return AQLM_ERR_ALIGN;
-  return status_of(aqlm::launch_dequant(L, w_out, static_cast<hipStream_t>(stream)));
+  return status_of(any_dequant(A, w_out, static_cast<hipStream_t>(stream)));
 }
 
 int aqlm_gemv(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
               int32_t M, int32_t B, int32_t g, const uint16_t* x, uint16_t* y, void* stream) {
-  aqlm::Layer L;
-  const int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L, true);
+  AnyLayer A;
+  const int st = check_any(codes, codebooks, scales, d_out, d_in, M, B, g, &A, true);
   if (st != AQLM_OK) return st;
   if (!x || !y) return AQLM_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return AQLM_ERR_ALIGN;
+  if (A.big) return status_of(aqlm::launch_gemv_groups(A.GL, x, y, static_cast<hipStream_t>(stream)));
+  const aqlm::Layer& L = A.L;
   if (L.packed && !aqlm::gemv_mfma_fits(&L, 1)) return AQLM_ERR_UNSUPPORTED;
   return status_of(gemv_dispatch(L, x, y, static_cast<hipStream_t>(stream)));
 }
@@ -231,12 +287,12 @@ extern "C" {
 int aqlm_gemm_small_batch(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                           int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
                           void* stream) {
-  aqlm::Layer L;
-  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  AnyLayer A;
+  int st = check_any(codes, codebooks, scales, d_out, d_in, M, B, g, &A);
   if (st != AQLM_OK) return st;
   st = check_tokens(x, y, n, d_in);
   if (st != AQLM_OK) return st;
-  return gemm_dispatch(L, n, x, y, static_cast<hipStream_t>(stream));
+  return any_gemm_dispatch(A, n, x, y, static_cast<hipStream_t>(stream));
 }
 
 size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n) {
@@ -250,22 +306,22 @@ size_t aqlm_gemm_workspace_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t
 int aqlm_gemm(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in,
               int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y, void* workspace,
               size_t workspace_bytes, void* stream) {
-  aqlm::Layer L;
-  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  AnyLayer A;
+  int st = check_any(codes, codebooks, scales, d_out, d_in, M, B, g, &A);
   if (st != AQLM_OK) return st;
   st = check_tokens(x, y, n, d_in);
   if (st != AQLM_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (!two_pass(d_in, n)) return gemm_dispatch(L, n, x, y, s);
+  if (!two_pass(d_in, n)) return any_gemm_dispatch(A, n, x, y, s);
   if (!workspace) return AQLM_ERR_NULL;
   const size_t wbytes = ws_weight_bytes(d_out, d_in);
   if (workspace_bytes < wbytes + aqlm::gemm_f16_part_bytes(n, d_out, d_in)) return AQLM_ERR_WORKSPACE;
   if (!aligned(workspace, 16)) return AQLM_ERR_ALIGN;
   uint16_t* w = static_cast<uint16_t*>(workspace);
   float* part = reinterpret_cast<float*>(static_cast<char*>(workspace) + wbytes);
-  const hipError_t e = aqlm::launch_dequant(L, w, s);
+  const hipError_t e = any_dequant(A, w, s);
   if (e != hipSuccess) return AQLM_ERR_HIP;
-  return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, L.d_out, L.d_in, s));
+  return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, (int32_t)A.d_out(), (int32_t)A.d_in(), s));
 }
 
 int aqlm_backward(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
@@ -301,22 +357,22 @@ int aqlm_beam_search(const float* w, const float* h, void* codes, const uint16_t
 int aqlm_gemm_noalloc(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                       int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x, uint16_t* y,
                       void* stream) {
-  aqlm::Layer L;
-  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  AnyLayer A;
+  int st = check_any(codes, codebooks, scales, d_out, d_in, M, B, g, &A);
   if (st != AQLM_OK) return st;
   st = check_tokens(x, y, n, d_in);
   if (st != AQLM_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (!two_pass(d_in, n)) return gemm_dispatch(L, n, x, y, s);
+  if (!two_pass(d_in, n)) return any_gemm_dispatch(A, n, x, y, s);
   const size_t wbytes = ws_weight_bytes(d_out, d_in);
   if (wbytes + aqlm::gemm_f16_part_bytes(n, d_out, d_in) > kScratchBytes) return AQLM_ERR_SCRATCH;
   char* base = static_cast<char*>(scratch_ptr());
   if (base == nullptr) return AQLM_ERR_HIP;
   uint16_t* w = reinterpret_cast<uint16_t*>(base);
   float* part = reinterpret_cast<float*>(base + wbytes);
-  const hipError_t e = aqlm::launch_dequant(L, w, s);
+  const hipError_t e = any_dequant(A, w, s);
   if (e != hipSuccess) return AQLM_ERR_HIP;
-  return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, L.d_out, L.d_in, s));
+  return status_of(aqlm::launch_gemm_f16(x, w, y, part, (int32_t)n, (int32_t)A.d_out(), (int32_t)A.d_in(), s));
 }
 
 int aqlm_gemv_grouped(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
@@ -329,6 +385,23 @@ int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int
   if (!problems) return AQLM_ERR_NULL;
   if (path != AQLM_PATH_AUTO && path != AQLM_PATH_GATHER && path != AQLM_PATH_TABLE) return AQLM_ERR_UNSUPPORTED;
   if (count < 1 || count > AQLM_MAX_GROUPED) return AQLM_ERR_SHAPE;
+  if (g != 8 && aqlm::groups_supported(M, B, g)) {
+    // larger groups: one group-kernel launch per problem (no grouped kernel)
+    if (path == AQLM_PATH_TABLE) return AQLM_ERR_UNSUPPORTED;
+    aqlm::GroupLayer GLs[AQLM_MAX_GROUPED];
+    for (int i = 0; i < count; ++i) {
+      const aqlm_gemv_problem& P = problems[i];
+      const int st = check_group_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &GLs[i]);
+      if (st != AQLM_OK) return st;
+      if (!P.x || !P.y) return AQLM_ERR_NULL;
+      if (!aligned(P.x, 16) || !aligned(P.y, 16)) return AQLM_ERR_ALIGN;
+    }
+    for (int i = 0; i < count; ++i) {
+      const hipError_t e = aqlm::launch_gemv_groups(GLs[i], problems[i].x, problems[i].y, static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) return AQLM_ERR_HIP;
+    }
+    return AQLM_OK;
+  }
   aqlm::Layer Ls[AQLM_MAX_GROUPED];
   const uint16_t* xs[AQLM_MAX_GROUPED];
   uint16_t* ys[AQLM_MAX_GROUPED];

@@ -324,3 +324,26 @@ def test_decode_step_launch_refusals(lib):
     assert lib.aqlm_gemv_step(ctypes.addressof(junk), P, P, 0, None) == SHAPE
     assert lib.aqlm_gemv_step_status(None, None) == NULL
     assert lib.aqlm_gemv_step_status(P + 4, None) == ALIGN
+
+
+def test_large_groups_accepted_only_where_supported(lib):
+    """g = 16, 32, 64 with 8-bit codes and up to 16 codebooks pass the checks
+    of the entry points that take them (the calls then stop at the fake
+    pointers' alignment); other shapes and entry points refuse them."""
+    for M, g in ((4, 16), (8, 32), (15, 64), (16, 64), (1, 16)):
+        assert deq(lib, M=M, g=g, d_in=128, w=P + 2) == ALIGN
+        assert gemv(lib, M=M, g=g, d_in=128, y=P + 2) == ALIGN
+        assert gemm(lib, M=M, g=g, d_in=128, y=P + 2) == ALIGN
+        assert gemm_ws(lib, M=M, g=g, d_in=128, y=P + 2) == ALIGN
+    for M, B, g in ((17, 8, 16), (4, 12, 16), (2, 16, 32), (4, 8, 128), (4, 8, 24), (0, 8, 16)):
+        assert gemv(lib, M=M, B=B, g=g, d_in=384) == UNSUP, (M, B, g)
+    assert gemv(lib, M=4, g=16, d_in=24) == SHAPE
+    assert lib.aqlm_backward(P, P, P, 64, 64, 4, 8, 16, 4, P, P, P, P, None) == UNSUP
+    assert lib.aqlm_beam_search(P, P, P, P, P, 8, 64, 4, 8, 16, 2, 1, P, None) == UNSUP
+    Prob = _lib.GemvProblem
+    arr = (Prob * 1)(Prob(P, P, P, P, P, 64, 64))
+    assert lib.aqlm_gemv_grouped_path(arr, 1, 4, 8, 16, _lib.PATH_TABLE, None) == UNSUP
+    nbytes = lib.aqlm_gemv_step_plan_bytes(1)
+    buf = ctypes.create_string_buffer(nbytes)
+    one = (ctypes.c_int32 * 1)(1)
+    assert lib.aqlm_gemv_step_plan(arr, one, 1, 4, 8, 16, ctypes.addressof(buf), nbytes) == UNSUP

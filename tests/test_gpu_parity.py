@@ -45,10 +45,10 @@ def check_products(lay, y_gpu, rows=None):
     error TOL of the oracle, and every element is within the bound its
     arithmetic allows (elementwise_bound)."""
     if rows is None:
-        w = oracle.dequantize(lay.codes, lay.codebooks, lay.scales)
+        w = oracle.dequantize(lay.codes, lay.codebooks, lay.scales, lay.g)
         got = y_gpu
     else:
-        w = oracle.dequantize_rows(lay.codes, lay.codebooks, lay.scales, rows)
+        w = oracle.dequantize_rows(lay.codes, lay.codebooks, lay.scales, rows, lay.g)
         got = y_gpu[:, rows]
     ref = oracle.matmul_f16(w, lay.x)
     assert np.all(np.isfinite(got.astype(np.float64)))
@@ -1221,3 +1221,83 @@ def test_decode_step_refuses_other_formats():
     y = torch.empty(64, dtype=torch.float16, device="cuda")
     with pytest.raises(aq().AqlmError):
         aq().DecodeStep([[(codes, cb, sc, x[0], y)]])
+
+
+# ------------------------------ larger groups (codebooks-versus-groups ablation)
+# 4x8 with groups of 16, 8x8 with 32, 15x8 with 64 (about two bits per weight)
+
+GROUP_FORMATS = [(4, 16), (8, 32), (15, 64)]
+
+
+@pytest.mark.parametrize("M,g", GROUP_FORMATS + [(1, 16), (3, 32), (16, 64)])
+@pytest.mark.parametrize("d_out,d_in", [(300, 1024), (37, 192), (1, 64), (1000, 4096)])
+def test_large_groups_dequantize_bit_exact(M, g, d_out, d_in):
+    print(f"[groups dequant] {M}x8 g{g} {d_out}x{d_in}", flush=True)
+    lay = synth.layer(26_000 + M + g + d_out, d_out, d_in, M, 8, g=g)
+    assert_bits_equal(dequant_gpu(lay), oracle.dequantize(lay.codes, lay.codebooks, lay.scales, g),
+                      "large-group dequantize")
+
+
+def test_large_groups_dequantize_special_values_bit_exact():
+    lay = synth.special_layer(26_100, 129, 256, 4, 8, g=16)
+    ref = oracle.dequantize(lay.codes, lay.codebooks, lay.scales, 16)
+    assert_bits_equal(dequant_gpu(lay), ref, "large-group dequantize special")
+    assert np.any(ref == 0x8000) and np.any((ref & 0x7C00) == 0)
+
+
+@pytest.mark.parametrize("M,g", GROUP_FORMATS)
+@pytest.mark.parametrize("d_out,d_in", [(4096, 4096), (11008, 4096), (4096, 11008), (37, 192)])
+def test_large_groups_gemv_matches_oracle(M, g, d_out, d_in):
+    """Codebooks in LDS (4x8 gs16 32 KiB, 8x8 gs32 128 KiB) or gathered from
+    L2 (15x8 gs64, 480 KiB); one wave per row."""
+    print(f"[groups gemv] {M}x8 g{g} {d_out}x{d_in}", flush=True)
+    lay = synth.layer(26_200 + M + g + d_out + d_in, d_out, d_in, M, 8, g=g)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().gemv(codes, cb, sc, x[0])
+    torch.cuda.synchronize()
+    check_products(lay, fp16_to_np(y)[None, :])
+
+
+@pytest.mark.parametrize("M,g", GROUP_FORMATS)
+def test_large_groups_grouped_small_batch_and_workspace(M, g):
+    """Grouped launches (one product per problem), n rows through the small-
+    batch entry point (one product per row), and the workspace product
+    (dequantize, then the dense product) at 64 and 300 rows; the no-
+    allocation variant bit for bit as the workspace product."""
+    print(f"[groups gemm] {M}x8 g{g}", flush=True)
+    lays = [synth.layer(26_300 + M + g + i, 500 + 64 * i, 1024, M, 8, g=g) for i in range(2)]
+    probs = []
+    for lay in lays:
+        codes, cb, sc, x = to_device(lay)
+        probs.append((codes, cb, sc, x[0], torch.full((lay.d_out,), float("nan"), dtype=torch.float16,
+                                                      device="cuda")))
+    aq().gemv_grouped(probs)
+    torch.cuda.synchronize()
+    for lay, p in zip(lays, probs):
+        check_products(lay, fp16_to_np(p[4])[None, :])
+    for n in (3, 64, 300):
+        lay = synth.layer(26_400 + M + g + n, 700, 1024, M, 8, n=n, g=g)
+        codes, cb, sc, x = to_device(lay)
+        y1 = aq().gemm_small_batch(codes, cb, sc, x)
+        y2 = aq().gemm(codes, cb, sc, x)
+        torch.cuda.synchronize()
+        check_products(lay, fp16_to_np(y1))
+        check_products(lay, fp16_to_np(y2))
+
+
+def test_large_groups_refused_elsewhere():
+    """Entry points without a large-group path refuse before launching."""
+    lay = synth.layer(26_500, 64, 256, 4, 8, n=4, g=16)
+    codes, cb, sc, x = to_device(lay)
+    y = torch.zeros(64, dtype=torch.float16, device="cuda")
+    with pytest.raises(aq().AqlmError):
+        aq().gemv_grouped([(codes, cb, sc, x[0], y)], path="table")
+    dcb = torch.zeros(tuple(cb.shape), dtype=torch.float32, device="cuda")
+    with pytest.raises(aq().AqlmError):
+        aq().backward(codes, cb, sc, x, torch.zeros((4, 64), dtype=torch.float16, device="cuda"), dcodebooks=dcb)
+    w = torch.zeros((64, 256), dtype=torch.float32, device="cuda")
+    h = torch.eye(256, dtype=torch.float32, device="cuda")
+    with pytest.raises(aq().AqlmError):
+        aq().beam_search(w, h, codes, cb, sc, beam=2)
+    torch.cuda.synchronize()
+    assert not y.any()
