@@ -221,7 +221,11 @@ hipError_t run_grad(const BwArgs& a, hipStream_t s) {
   auto kern = k_grad_cb<M>;
   const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(kern), (int)lds);
   if (e != hipSuccess) return e;
-  const int per_cu = lds * 2 <= 160 * 1024 ? 2 : 1;
+  // persistent workgroups: as many as can be resident at once (registers
+  // and LDS), so that none waits for another to finish all of its tiles
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kBwThreads, lds) != hipSuccess || per_cu < 1)
+    per_cu = 1;
   int grid = num_cus() * per_cu;
   if (grid > a.tiles) grid = a.tiles;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(kBwThreads), lds, s, a);
