@@ -88,6 +88,8 @@ def parse_args():
                     help="only time the gradients through Eq. 2 (aqlm_backward) and exit")
     ap.add_argument("--persistent", action="store_true",
                     help="only the workload's step as one persistent launch (aqlm_gemv_step) beside its graph")
+    ap.add_argument("--sorted", action="store_true",
+                    help="only the workload's step (a 1x16 one) over chunk-sorted codes beside its graph")
     ap.add_argument("--single-layers", action="store_true",
                     help="only the single-layer matrix-vector rows (incl. bit-packed codes)")
     ap.add_argument("--beam-search", action="store_true",
@@ -405,6 +407,14 @@ def single_layer_rows(aq, torch):
         "11008x4096 2x15 packed": (11008, 4096, 2, 15),
         "11008x4096 1x15 packed": (11008, 4096, 1, 15),
         "4096x4096 2x12 packed": (4096, 4096, 2, 12),
+        # chunk-sorted codes (aqlm_gemv_sorted)
+        "4096x4096 1x16 sorted": (4096, 4096, 1, 16),
+        "11008x4096 1x16 sorted": (11008, 4096, 1, 16),
+        "4096x11008 1x16 sorted": (4096, 11008, 1, 16),
+        "28672x8192 1x16 sorted": (28672, 8192, 1, 16),
+        "8192x28672 1x16 sorted": (8192, 28672, 1, 16),
+        "11008x4096 2x16 sorted": (11008, 4096, 2, 16),
+        "11008x4096 1x15 sorted": (11008, 4096, 1, 15),
         # larger groups (about two bits per weight, like 2x8)
         "4096x4096 4x8 gs16": (4096, 4096, 4, 8),
         "4096x4096 8x8 gs32": (4096, 4096, 8, 8),
@@ -416,8 +426,28 @@ def single_layer_rows(aq, torch):
         shp = fmt.AqlmShape(d_out, d_in, M, B, g)
         code_bytes = shp.packed_codes_bytes() if packed else shp.codes_bytes()
         reps = max(2, min(256, (1 << 30) // code_bytes + 1))
-        layers = [DeviceLayer(900000 + i, d_out, d_in, M, B, packed=packed, g=g) for i in range(reps)]
-        calls = [lambda L=L: L.gemv(aq) for L in layers]
+        sorted_ = name.endswith("sorted")
+        if sorted_:
+            # one layer sorted on the host, its sorted arrays copied per replica
+            import copy
+            src = DeviceLayer(900000, d_out, d_in, M, B)
+            base = aq.SortedCodes(src.codes, src.codebooks, src.scales)
+            sbytes = base.entries.numel() * 4
+            reps = max(2, min(256, (1 << 30) // sbytes + 1))
+            layers = []
+            for i in range(reps):
+                c = copy.copy(base)
+                c.entries, c.index = base.entries.clone(), base.index.clone()
+                c.codebooks = src.codebooks.clone()
+                layers.append(c)
+            ws = base.workspace
+            x0, y0 = src.x[0], src.y[0]
+            calls = [lambda c=c: c.gemv(x0, out=y0) for c in layers]
+            for c in layers:
+                c.workspace = ws
+        else:
+            layers = [DeviceLayer(900000 + i, d_out, d_in, M, B, packed=packed, g=g) for i in range(reps)]
+            calls = [lambda L=L: L.gemv(aq) for L in layers]
         g = graph_of(calls)
         ms = time_steps(g.replay, steps=3, warmup=1) / reps
         pair = per_launch_ms(calls[: min(reps, 64)], reps=2)
@@ -425,9 +455,15 @@ def single_layer_rows(aq, torch):
         del g
         b = shp.packed_gemv_bytes(1) if packed else shp.gemv_bytes(1)
         pb = shp.paper_gemv_bytes(1)  # codes at B bits each
-        rows.append({"layer": name, "bytes": b, "paper_bytes": pb, "GBs_paper_bytes": pb / (ms * 1e6), "us_per_call": ms * 1e3, "frac_per_call": b / (ms * 1e6) / HBM_PEAK_GBS,
-                     "GBs_per_call": b / (ms * 1e6), "event_pair_us": pair_ms * 1e3,
-                     "GBs_event_pair": b / (pair_ms * 1e6), "replicas": reps})
+        row = {"layer": name, "bytes": b, "paper_bytes": pb, "GBs_paper_bytes": pb / (ms * 1e6),
+               "us_per_call": ms * 1e3, "frac_per_call": b / (ms * 1e6) / HBM_PEAK_GBS,
+               "GBs_per_call": b / (ms * 1e6), "event_pair_us": pair_ms * 1e3,
+               "GBs_event_pair": b / (pair_ms * 1e6), "replicas": reps}
+        if sorted_:
+            # bytes the sorted product streams (entries: 4 per code plus pads)
+            row["sorted_entry_bytes"] = sbytes
+            row["GBs_sorted_entries"] = sbytes / (ms * 1e6)
+        rows.append(row)
         del layers
         torch.cuda.empty_cache()
     return rows
@@ -645,6 +681,38 @@ def persistent_step_row(layers, graph, aq, torch, steps, step_bytes, graph_ms):
             "levels": len(levels), "launches": 1, "vs_graph": graph_ms / ms, "bit_identical_to_graph": same}
 
 
+def sorted_step_row(layers, aq, torch, steps, step_bytes, graph_ms):
+    """The 1x16 decode step over chunk-sorted codes (aqlm_gemv_sorted):
+    grouped q/k/v, o, grouped gate/up, down, as one graph; outputs compared
+    with the row-major graph's (relative L2)."""
+    import time
+    t0 = time.time()
+    srt = [aq.SortedCodes(L.codes, L.codebooks, L.scales) for L in layers]
+    sort_s = time.time() - t0
+    entry_bytes = sum(s.entries.numel() * 4 + s.index.numel() * 4 for s in srt)
+    rows = max(sum(L.shape.d_out for L in layers[b:b + 3]) for b in range(0, len(layers), 7))
+    rows = max(rows, max(sum(L.shape.d_out for L in layers[b + 4:b + 6]) for b in range(0, len(layers), 7)))
+    ws = torch.zeros((aq._lib.load().aqlm_gemv_sorted_workspace_bytes(rows, 1, 16),), dtype=torch.uint8,
+                     device="cuda")
+    ref = [L.y.clone() for L in layers]
+    launches = []
+    for b in range(0, len(layers), 7):
+        q, k, v, o, gate, up, down = [(srt[b + i], layers[b + i]) for i in range(7)]
+        grp = lambda items: (lambda: aq.gemv_sorted_grouped([(s, L.x[0], L.y[0]) for s, L in items], workspace=ws))
+        launches += [grp([q, k, v]), grp([o]), grp([gate, up]), grp([down])]
+    g = graph_of(launches)
+    g.replay()
+    torch.cuda.synchronize()
+    err = max(float(torch.linalg.norm((L.y.float() - r.float())) / max(float(torch.linalg.norm(r.float())), 1e-30))
+              for L, r in zip(layers, ref))
+    ms = time_steps(g.replay, steps, 2)
+    del g, srt, ref
+    return {"ms_per_step": ms, "GBs": step_bytes / (ms * 1e6), "frac": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
+            "tok_s_eq": 1000.0 / ms, "launches": len(launches), "vs_row_major_graph": graph_ms / ms,
+            "sorted_bytes_per_step": entry_bytes, "GBs_sorted_bytes": entry_bytes / (ms * 1e6),
+            "host_sort_s": sort_s, "max_rel_l2_vs_row_major": err}
+
+
 def step_seed(M: int) -> int:
     return 1000 * (1 if M == 2 else 2)
 
@@ -689,6 +757,14 @@ def main():
                                                                       args.warmup)
         row = persistent_step_row(layers, graph, aq, torch, args.steps, step_bytes, ms)
         print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "persistent_step": row}), flush=True)
+        return
+    if args.sorted:
+        if B < 15:
+            sys.exit("bench.py: --sorted needs a workload with 15- or 16-bit codes (llama2-7b-1x16)")
+        layers, launches, graph, ms, spread, step_bytes = decode_step(model, M, B, step_seed(M), aq, args.steps,
+                                                                      args.warmup)
+        row = sorted_step_row(layers, aq, torch, args.steps, step_bytes, ms)
+        print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "sorted_codes": row}), flush=True)
         return
     layers, launches, graph, ms, spread, step_bytes = decode_step(
         model, M, B, step_seed(M), aq, args.steps, args.warmup, markers=True)
@@ -792,6 +868,9 @@ def main():
                 row["independent_8_per_launch"] = {"launches": len(fused), "ms_per_step": ms8,
                                                    "GBs": ob / (ms8 * 1e6)}
                 del g1, g8
+            if oM == 1:
+                row["sorted_codes"] = sorted_step_row(ol, aq, torch, max(5, args.steps // 2), ob, oms)
+                log(f"{other} over sorted codes: {row['sorted_codes']['ms_per_step']:.4f} ms per step")
             sec[other] = row
             del ol, olaunch, og
             torch.cuda.empty_cache()

@@ -331,6 +331,109 @@ int aqlm_gemv_step(const void* plan_host, const void* plan_dev, void* sync, uint
  * up, AQLM_OK otherwise. */
 int aqlm_gemv_step_status(void* sync, void* stream);
 
+/* ------------------------------------------------------- chunk-sorted codes
+ *
+ * A second storage of the codes of the formats with large codebooks - one or
+ * two codebooks of 2^15 or 2^16 codewords, g = 8 (the 2- and 4-bit settings
+ * of the appendix "Experimental Configurations") - for the matrix-vector
+ * product (Sec. 4.3).  Such a codebook (1 MiB for 2^16 fp16 codewords of 8)
+ * does not fit on chip, so with row-major codes every code fetches its
+ * codeword from the L2 cache.  The sorted form lists, for every block of 16
+ * output rows, the block's codes chunk by chunk (a chunk is 8192 consecutive
+ * codewords of one codebook, 128 KiB), so that the product can stage one
+ * chunk per workgroup on chip and serve each code from there.  Eq. 2 and the
+ * product are unchanged; only the order in which codes are read changes.
+ *
+ * Layout (K = M * 2^(B-13) chunk classes; code (i, j, m) of value v is in
+ * class c = m * 2^(B-13) + (v >> 13); nb = ceil(d_out / 16) row blocks):
+ *   index    uint32 [K * nb + 1]: index[c * nb + b] = first step of the list
+ *            of class c in block b; index[K * nb] = total steps.  The list has
+ *            ceil(n / 4) steps, n the largest number of class-c codes of one
+ *            row of the block.
+ *   entries  uint32 [total steps * 64]: the k-th class-c code (ascending j)
+ *            of row 16 b + i is entry 64 * (index[c * nb + b] + k / 4)
+ *            + 16 * (k % 4) + i, stored as (v & 8191) | (j << 14); every other
+ *            entry is the pad 0xFFFFE000, which adds nothing.
+ * The sorted form takes about 2.5 times the bytes of 16-bit codes (4 bytes
+ * per code, and pads up to the longest row of each block); the row-major
+ * codes stay the input of every other entry point. */
+
+/* Sizes of the sorted form of `codes_host` (HOST memory; layout as for
+ * aqlm_gemv, unpacked uint16 or bit-packed with B | AQLM_PACKED):
+ * *entry_words = total steps * 64, *index_words = K * nb + 1.  Reads every
+ * code.  Supported: M = 1 or 2, B = 15 or 16, g = 8 (else
+ * AQLM_ERR_UNSUPPORTED); d_in / 8 at most 262142 and the entries below 2 GiB
+ * (else AQLM_ERR_SHAPE). */
+int aqlm_sort_codes_size(const void* codes_host, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                         int64_t* entry_words, int64_t* index_words);
+
+/* Writes the sorted form of `codes_host` into HOST arrays entries_host
+ * [entry_words] and index_host [index_words] (at least the sizes above, else
+ * AQLM_ERR_WORKSPACE).  Runs on the host (once per layer, when it is loaded);
+ * the caller copies both arrays to the device for aqlm_gemv_sorted.
+ * Deterministic. */
+int aqlm_sort_codes(const void* codes_host, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                    uint32_t* entries_host, int64_t entry_words, uint32_t* index_host, int64_t index_words);
+
+/* Device workspace of aqlm_gemv_sorted in bytes: 4096 bytes of counters,
+ * then one 8-byte (partial sum, launch tag) word per chunk class and output
+ * row (K * d_out * 8); for aqlm_gemv_sorted_grouped pass the sum of the
+ * problems' d_out.  0 for an unsupported format or size. */
+size_t aqlm_gemv_sorted_workspace_bytes(int64_t d_out, int32_t M, int32_t B);
+
+/* The matrix-vector product of aqlm_gemv over sorted codes (entries, index:
+ * DEVICE copies of what aqlm_sort_codes wrote for this layer; entry_words:
+ * their count; index_host: the HOST array aqlm_sort_codes wrote, or NULL - when
+ * given, the workgroups' first steps travel with the launch arguments instead
+ * of being read from the device index first, which saves a memory round trip
+ * per launch; it must hold the same values as `index`): y[i] = fp16(s_i * sum_j sum_m <C_m[b[i][j][m]], x[j*8 ..
+ * j*8+8)>), fp32 accumulation.  One workgroup per (chunk class, range of row
+ * blocks) stages its codebook chunk on chip; the K class sums of a row are
+ * added in class order by one workgroup of its range, then scaled and rounded
+ * once.  Deterministic; agrees with aqlm_gemv to fp32 accumulation accuracy
+ * (the summation order differs).
+ *   workspace: DEVICE memory of at least aqlm_gemv_sorted_workspace_bytes
+ *   bytes, 16-byte aligned, whose first 4096 bytes (counters) are zero before
+ *   its first use.  Every launch adds to the counters it uses and leaves them
+ *   consistent, so one workspace, sized for the largest launch, serves any
+ *   sequence of calls, for any layers and formats, on one stream; calls that
+ *   may overlap (other streams) need their own workspace.  A workspace whose
+ *   counters were disturbed can make the summing workgroup give up waiting
+ *   for a partial sum (after about 4M polls): the rows it sums are then NaN.
+ *   Entries and index are read, never written; an index or entries array that
+ *   does not belong to the layer gives wrong results but no access outside
+ *   the arrays (entry_words bounds every read).  Supported as for
+ *   aqlm_sort_codes, with d_out up to 6553600 (else AQLM_ERR_SHAPE); entries
+ *   and index 4-byte aligned, x 16-byte aligned, y 2-byte aligned. */
+int aqlm_gemv_sorted(const uint32_t* entries, int64_t entry_words, const uint32_t* index, const uint32_t* index_host,
+                     const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in, int32_t M,
+                     int32_t B, int32_t g, const uint16_t* x, uint16_t* y, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+/* One problem of a grouped sorted launch (device pointers; as aqlm_gemv_sorted). */
+typedef struct aqlm_sorted_problem {
+  const uint32_t* entries;
+  int64_t entry_words;
+  const uint32_t* index;
+  const uint32_t* index_host; /* HOST copy of index, or NULL (see aqlm_gemv_sorted) */
+  const uint16_t* codebooks;
+  const uint16_t* scales;
+  const uint16_t* x; /* [d_in] */
+  uint16_t* y;       /* [d_out] */
+  int64_t d_out;
+  int64_t d_in;
+} aqlm_sorted_problem;
+
+/* `count` (1..AQLM_MAX_GROUPED) sorted products of one format in one launch
+ * (q, k, v or gate, up projections), each computed as aqlm_gemv_sorted
+ * computes it; the workgroups are dealt to the problems by their entries.
+ * `problems` is a HOST array read during the call; every problem is validated
+ * before anything is launched.  Workspace: aqlm_gemv_sorted_workspace_bytes of
+ * the summed d_out.  Deterministic; results may differ from separate calls in
+ * the last bits (the row ranges differ). */
+int aqlm_gemv_sorted_grouped(const aqlm_sorted_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static text for a status code (never NULL). */
 const char* aqlm_status_string(int status);
 

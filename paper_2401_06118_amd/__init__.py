@@ -15,7 +15,10 @@ Eq. 2 and Fig. 3).  This package exposes the three operations of the C ABI in
 - :func:`beam_search` - Phase 1 of the quantizer: beam search over the codes;
 - :class:`DecodeStep` - the products of a whole decode step (levels of
   grouped 2x8 products, each level free to read what earlier ones wrote) as
-  one persistent launch.
+  one persistent launch;
+- :class:`SortedCodes` - a chunk-sorted copy of the codes of the large-codebook
+  formats (1x15, 1x16, 2x15, 2x16) whose matrix-vector product serves every
+  code from a codebook chunk held on chip.
 
 Every computation runs in the hand-written HIP kernels of
 ``libaqlm_mi355x.so``; this module only marshals arguments.
@@ -30,13 +33,15 @@ to whole 32-bit words (``format.pack_codes`` writes it).
 """
 from __future__ import annotations
 
+import ctypes
+
 import torch
 
 from . import _lib
 from ._lib import AqlmError, status_string  # noqa: F401
 
 __all__ = ["dequantize", "gemv", "gemv_grouped", "gemm_small_batch", "gemm_workspace_bytes", "gemm", "backward",
-           "beam_search", "DecodeStep",
+           "beam_search", "DecodeStep", "SortedCodes", "gemv_sorted_grouped",
            "AqlmError",
            "status_string", "layer_args", "packed_layer_args"]
 
@@ -328,3 +333,94 @@ class DecodeStep:
         of an earlier run gave up (the flag is cleared)."""
         _check(_lib.load().aqlm_gemv_step_status(self.sync.data_ptr(), _stream_handle(stream)),
                "aqlm_gemv_step_status")
+
+
+class SortedCodes:
+    """Chunk-sorted copy of a layer's codes for the matrix-vector product
+    (``aqlm_sort_codes`` / ``aqlm_gemv_sorted``).
+
+    For one or two codebooks of 2^15 or 2^16 codewords: the codes of every
+    16-row block are regrouped by 8192-codeword chunk on the host, once, and
+    the entries, their index and a zeroed workspace are kept on the layer's
+    device.  :meth:`gemv` then computes what :func:`gemv` computes for the
+    original codes.  ``codes``: the layer's codes as for :func:`gemv`
+    (uint16/int16 [d_out, d_in/8, M], or bit-packed int32 with ``d_in``).
+    Calls on one stream may share the object; calls on several streams at
+    once need one object each (the workspace is shared)."""
+
+    def __init__(self, codes, codebooks, scales, *, d_in=None):
+        d_out, d_in, M, B, g = _args(codes, codebooks, scales, d_in)
+        lib = _lib.load()
+        host = codes.detach().to("cpu").contiguous()
+        ew, iw = ctypes.c_int64(0), ctypes.c_int64(0)
+        _check(lib.aqlm_sort_codes_size(host.data_ptr(), d_out, d_in, M, B, g, ctypes.byref(ew),
+                                        ctypes.byref(iw)), "aqlm_sort_codes_size")
+        entries = torch.empty(ew.value, dtype=torch.int32)
+        index = torch.empty(iw.value, dtype=torch.int32)
+        _check(lib.aqlm_sort_codes(host.data_ptr(), d_out, d_in, M, B, g, entries.data_ptr(), ew.value,
+                                   index.data_ptr(), iw.value), "aqlm_sort_codes")
+        dev = codes.device
+        self.entries = entries.to(dev)
+        self.index = index.to(dev)
+        self.index_host = index  # (lets a launch carry the workgroups' first steps)
+        self.codebooks, self.scales = codebooks, scales
+        self.d_out, self.d_in, self.M, self.B, self.g = d_out, d_in, M, B & ~_lib.PACKED, g
+        need = int(lib.aqlm_gemv_sorted_workspace_bytes(d_out, M, self.B))
+        # (zero counters before the first launch; launches keep them consistent)
+        self.workspace = torch.zeros((need,), dtype=torch.uint8, device=dev)
+
+    def gemv(self, x, *, out=None, stream=None) -> torch.Tensor:
+        """y = W x for x fp16 [d_in] on the GPU (as :func:`gemv`)."""
+        if x.dtype != torch.float16 or x.numel() != self.d_in or not x.is_cuda or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
+        out = _out(out, (self.d_out,), self.entries)
+        st = _lib.load().aqlm_gemv_sorted(
+            self.entries.data_ptr(), self.entries.numel(), self.index.data_ptr(), self.index_host.data_ptr(),
+            self.codebooks.data_ptr(),
+            self.scales.data_ptr(), self.d_out, self.d_in, self.M, self.B, self.g, x.data_ptr(), out.data_ptr(),
+            self.workspace.data_ptr(), self.workspace.numel(), _stream_handle(stream))
+        _check(st, "aqlm_gemv_sorted")
+        return out
+
+
+_sorted_ws = {}
+
+
+def _sorted_workspace(device, need: int) -> torch.Tensor:
+    """A zeroed workspace of at least ``need`` bytes for grouped sorted
+    launches on ``device`` (kept and grown between calls)."""
+    ws = _sorted_ws.get(device)
+    if ws is None or ws.numel() < need:
+        ws = torch.zeros((need,), dtype=torch.uint8, device=device)
+        _sorted_ws[device] = ws
+    return ws
+
+
+def gemv_sorted_grouped(problems, *, workspace=None, stream=None):
+    """Several sorted products of one format in one launch
+    (``aqlm_gemv_sorted_grouped``): ``problems`` is a list of
+    (:class:`SortedCodes`, x fp16 [d_in], y fp16 [d_out]) on one GPU.  Without
+    ``workspace`` a zeroed one kept per device is used (calls on several
+    streams at once need their own)."""
+    if not 1 <= len(problems) <= _lib.MAX_GROUPED:
+        raise ValueError(f"1..{_lib.MAX_GROUPED} problems")
+    first = problems[0][0]
+    arr = (_lib.SortedProblem * len(problems))()
+    rows = 0
+    for k, (sc, x, y) in enumerate(problems):
+        if (sc.M, sc.B, sc.g) != (first.M, first.B, first.g):
+            raise ValueError("grouped problems must share (M, B, g)")
+        if x.dtype != torch.float16 or x.numel() != sc.d_in or not x.is_cuda or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
+        _out(y, (sc.d_out,), sc.entries)
+        arr[k] = _lib.SortedProblem(sc.entries.data_ptr(), sc.entries.numel(), sc.index.data_ptr(),
+                                    sc.index_host.data_ptr(), sc.codebooks.data_ptr(), sc.scales.data_ptr(), x.data_ptr(), y.data_ptr(),
+                                    sc.d_out, sc.d_in)
+        rows += sc.d_out
+    lib = _lib.load()
+    need = int(lib.aqlm_gemv_sorted_workspace_bytes(rows, first.M, first.B))
+    if workspace is None:
+        workspace = _sorted_workspace(first.entries.device, need)
+    st = lib.aqlm_gemv_sorted_grouped(arr, len(problems), first.M, first.B, first.g, workspace.data_ptr(),
+                                      workspace.numel() * workspace.element_size(), _stream_handle(stream))
+    _check(st, "aqlm_gemv_sorted_grouped")

@@ -22,7 +22,8 @@ PATH_AUTO, PATH_GATHER, PATH_TABLE = 0, 1, 2
 EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemv_grouped_path", "aqlm_gemm_small_batch",
            "aqlm_gemm_workspace_bytes", "aqlm_gemm", "aqlm_gemm_noalloc", "aqlm_backward", "aqlm_beam_search",
            "aqlm_packed_row_words", "aqlm_gemv_step_plan_bytes", "aqlm_gemv_step_plan", "aqlm_gemv_step",
-           "aqlm_gemv_step_status", "aqlm_status_string")
+           "aqlm_gemv_step_status", "aqlm_sort_codes_size", "aqlm_sort_codes", "aqlm_gemv_sorted_workspace_bytes",
+           "aqlm_gemv_sorted", "aqlm_gemv_sorted_grouped", "aqlm_status_string")
 MAX_GROUPED = 8
 PACKED = 0x100  # OR-ed into B: bit-packed codes
 STEP_SYNC_BYTES = 256
@@ -33,6 +34,13 @@ class GemvProblem(ctypes.Structure):
     _fields_ = [("codes", ctypes.c_void_p), ("codebooks", ctypes.c_void_p), ("scales", ctypes.c_void_p),
                 ("x", ctypes.c_void_p), ("y", ctypes.c_void_p), ("d_out", ctypes.c_int64),
                 ("d_in", ctypes.c_int64)]
+
+class SortedProblem(ctypes.Structure):
+    """Mirror of ``aqlm_sorted_problem`` in include/aqlm.h."""
+    _fields_ = [("entries", ctypes.c_void_p), ("entry_words", ctypes.c_int64), ("index", ctypes.c_void_p),
+                ("index_host", ctypes.c_void_p), ("codebooks", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("x", ctypes.c_void_p),
+                ("y", ctypes.c_void_p), ("d_out", ctypes.c_int64), ("d_in", ctypes.c_int64)]
+
 
 _lock = threading.Lock()
 _lib = None
@@ -89,6 +97,18 @@ def load():
         lib.aqlm_gemv_step.restype = ctypes.c_int
         lib.aqlm_gemv_step_status.argtypes = [p, p]
         lib.aqlm_gemv_step_status.restype = ctypes.c_int
+        lib.aqlm_sort_codes_size.argtypes = [p, i64, i64, i32, i32, i32, ctypes.POINTER(ctypes.c_int64),
+                                             ctypes.POINTER(ctypes.c_int64)]
+        lib.aqlm_sort_codes_size.restype = ctypes.c_int
+        lib.aqlm_sort_codes.argtypes = [p, i64, i64, i32, i32, i32, p, i64, p, i64]
+        lib.aqlm_sort_codes.restype = ctypes.c_int
+        lib.aqlm_gemv_sorted_workspace_bytes.argtypes = [i64, i32, i32]
+        lib.aqlm_gemv_sorted_workspace_bytes.restype = ctypes.c_size_t
+        lib.aqlm_gemv_sorted.argtypes = [p, i64, p, p, p, p, i64, i64, i32, i32, i32, p, p, p, ctypes.c_size_t, p]
+        lib.aqlm_gemv_sorted.restype = ctypes.c_int
+        lib.aqlm_gemv_sorted_grouped.argtypes = [ctypes.POINTER(SortedProblem), i32, i32, i32, i32, p,
+                                                 ctypes.c_size_t, p]
+        lib.aqlm_gemv_sorted_grouped.restype = ctypes.c_int
         lib.aqlm_status_string.argtypes = [ctypes.c_int]
         lib.aqlm_status_string.restype = ctypes.c_char_p
         _lib = lib

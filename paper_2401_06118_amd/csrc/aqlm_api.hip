@@ -12,6 +12,7 @@
 #include "../../include/aqlm.h"
 #include "groups.h"
 #include "launch.h"
+#include "sorted.h"
 
 namespace aqlm {
 
@@ -511,6 +512,109 @@ int aqlm_gemv_step_status(void* sync, void* stream) {
   const uint32_t zero = 0;
   if (hipMemcpy(flag, &zero, sizeof(zero), hipMemcpyHostToDevice) != hipSuccess) return AQLM_ERR_HIP;
   return AQLM_ERR_TIMEOUT;
+}
+
+// Chunk-sorted codes: the shape and format rules shared by the sorter and
+// the product.
+static int check_sorted_shape(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g) {
+  if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return AQLM_ERR_SHAPE;
+  if (g != 8 || !aqlm::sorted_supported(M, B)) return AQLM_ERR_UNSUPPORTED;
+  const int64_t G = d_in / g;
+  if (d_out >= (int64_t(1) << 31) || d_out * G >= (int64_t(1) << 31) || G > (int64_t)aqlm::kSortedJMax)
+    return AQLM_ERR_SHAPE;
+  return AQLM_OK;
+}
+
+// (entries are addressed in bytes with 32 bits on the device)
+static constexpr int64_t kSortedMaxSteps = (int64_t(1) << 31) / 256 - 1;
+
+static int sort_input(const void* codes, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, bool* packed,
+                      int64_t* steps) {
+  if (!codes) return AQLM_ERR_NULL;
+  *packed = (B & AQLM_PACKED) != 0;
+  const int32_t b = B & ~AQLM_PACKED;
+  int st = check_sorted_shape(d_out, d_in, M, b, g);
+  if (st != AQLM_OK) return st;
+  if (*packed && !aqlm::packed_supported(M, b)) return AQLM_ERR_UNSUPPORTED;
+  if (*packed && (d_in / g) * M * b >= (int64_t(1) << 32)) return AQLM_ERR_SHAPE;
+  *steps = aqlm::sorted_steps(codes, *packed, (int32_t)d_out, (int32_t)d_in, M, b);
+  if (*steps > kSortedMaxSteps) return AQLM_ERR_SHAPE;
+  return AQLM_OK;
+}
+
+int aqlm_sort_codes_size(const void* codes_host, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                         int64_t* entry_words, int64_t* index_words) {
+  if (!entry_words || !index_words) return AQLM_ERR_NULL;
+  bool packed = false;
+  int64_t steps = 0;
+  const int st = sort_input(codes_host, d_out, d_in, M, B, g, &packed, &steps);
+  if (st != AQLM_OK) return st;
+  *entry_words = steps * 64;
+  *index_words = (int64_t)aqlm::sorted_classes(M, B & ~AQLM_PACKED) * aqlm::sorted_blocks(d_out) + 1;
+  return AQLM_OK;
+}
+
+int aqlm_sort_codes(const void* codes_host, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g,
+                    uint32_t* entries_host, int64_t entry_words, uint32_t* index_host, int64_t index_words) {
+  if (!entries_host || !index_host) return AQLM_ERR_NULL;
+  bool packed = false;
+  int64_t steps = 0;
+  const int st = sort_input(codes_host, d_out, d_in, M, B, g, &packed, &steps);
+  if (st != AQLM_OK) return st;
+  const int32_t b = B & ~AQLM_PACKED;
+  if (entry_words < steps * 64 ||
+      index_words < (int64_t)aqlm::sorted_classes(M, b) * aqlm::sorted_blocks(d_out) + 1)
+    return AQLM_ERR_WORKSPACE;
+  aqlm::sort_codes(codes_host, packed, (int32_t)d_out, (int32_t)d_in, M, b, entries_host, steps, index_host);
+  return AQLM_OK;
+}
+
+size_t aqlm_gemv_sorted_workspace_bytes(int64_t d_out, int32_t M, int32_t B) {
+  if (d_out <= 0 || d_out >= (int64_t(1) << 31) || !aqlm::sorted_supported(M, B)) return 0;
+  return aqlm::gemv_sorted_workspace_bytes(d_out, M, B);
+}
+
+static int check_sorted_problem(const aqlm_sorted_problem& P, int32_t M, int32_t B, int32_t g,
+                                aqlm::SortedLayer* L) {
+  if (!P.entries || !P.index || !P.codebooks || !P.scales || !P.x || !P.y) return AQLM_ERR_NULL;
+  const int st = check_sorted_shape(P.d_out, P.d_in, M, B, g);
+  if (st != AQLM_OK) return st;
+  if (P.entry_words <= 0 || P.entry_words % 64 != 0 || P.entry_words / 64 > kSortedMaxSteps) return AQLM_ERR_SHAPE;
+  if (!aligned(P.entries, 4) || !aligned(P.index, 4) || !aligned(P.codebooks, 16) || !aligned(P.scales, 2) ||
+      !aligned(P.x, 16) || !aligned(P.y, 2))
+    return AQLM_ERR_ALIGN;
+  *L = aqlm::SortedLayer{P.entries, P.index, P.index_host, P.entry_words / 64, P.codebooks, P.scales,
+                         (int32_t)P.d_out, (int32_t)P.d_in, M, B};
+  return AQLM_OK;
+}
+
+int aqlm_gemv_sorted_grouped(const aqlm_sorted_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  if (!problems || !workspace) return AQLM_ERR_NULL;
+  if (count < 1 || count > AQLM_MAX_GROUPED) return AQLM_ERR_SHAPE;
+  aqlm::SortedLayer Ls[AQLM_MAX_GROUPED];
+  const uint16_t* xs[AQLM_MAX_GROUPED];
+  uint16_t* ys[AQLM_MAX_GROUPED];
+  int64_t rows = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const int st = check_sorted_problem(problems[i], M, B, g, &Ls[i]);
+    if (st != AQLM_OK) return st;
+    xs[i] = problems[i].x;
+    ys[i] = problems[i].y;
+    rows += problems[i].d_out;
+  }
+  if (!aqlm::gemv_sorted_fits(Ls, count)) return AQLM_ERR_SHAPE;
+  if (!aligned(workspace, 16)) return AQLM_ERR_ALIGN;
+  if (workspace_bytes < aqlm::gemv_sorted_workspace_bytes(rows, M, B)) return AQLM_ERR_WORKSPACE;
+  return status_of(aqlm::launch_gemv_sorted(Ls, xs, ys, count, workspace, static_cast<hipStream_t>(stream)));
+}
+
+int aqlm_gemv_sorted(const uint32_t* entries, int64_t entry_words, const uint32_t* index, const uint32_t* index_host,
+                     const uint16_t* codebooks, const uint16_t* scales, int64_t d_out, int64_t d_in, int32_t M,
+                     int32_t B, int32_t g, const uint16_t* x, uint16_t* y, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  const aqlm_sorted_problem P{entries, entry_words, index, index_host, codebooks, scales, x, y, d_out, d_in};
+  return aqlm_gemv_sorted_grouped(&P, 1, M, B, g, workspace, workspace_bytes, stream);
 }
 
 int64_t aqlm_packed_row_words(int64_t d_in, int32_t M, int32_t B, int32_t g) {
