@@ -25,9 +25,16 @@ FLAGS = ["-std=c++17", "-O3", "-fPIC", f"--offload-arch={ARCH}",
          "-Wall", "-Wno-unused-command-line-argument"]
 
 
+# Per-file additions.  sorted.hip: one lane per workgroup takes a ticket with
+# a returning atomic whose value is needed only at the end of the kernel; the
+# atomic optimizer would aggregate it over the wave and read the result back
+# at once, which stalls the wave for a memory round trip before its barrier.
+FILE_FLAGS = {"sorted.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"]}
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

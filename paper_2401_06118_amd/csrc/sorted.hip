@@ -160,7 +160,7 @@ constexpr int kMaxBpr = 400;                  // most blocks of a row range (LDS
 constexpr uint32_t kTicket = 16;              // every launch adds 16 to the counter of each of its ranges
 constexpr uint32_t kSpin = 1u << 22;          // polls of a missing partial before giving up
 constexpr uint16_t kNaNh = 0x7E00;
-constexpr int kMaxBounds = 512;
+constexpr int kMaxBoundWgs = 256;
 
 struct SortedProblem {
   const uint32_t* entries;
@@ -178,7 +178,6 @@ struct SortedProblem {
   int32_t R;            // row ranges
   int32_t wg_begin;     // first workgroup (a multiple of K)
   int32_t range_begin;  // counter of its first range
-  int32_t bounds_at;    // its K * (R + 1) range bounds in SortedBatch::bounds (-1: read the index)
 };
 
 struct SortedBatch {
@@ -188,11 +187,22 @@ struct SortedBatch {
   int32_t B;
   int32_t bpr;       // most blocks of a range over the problems
   uint32_t seg_lds;  // byte offset of the segment sums in LDS (after the chunk and x)
-  // first step of class c's lists of range r, at bounds_at + c * (R + 1) + r,
-  // from the caller's host copy of the index: read with the other arguments,
-  // so the first entry loads need not wait for the index
-  uint32_t bounds[kMaxBounds];
+  // every workgroup's steps [first, end), at 2 * blockIdx.x, from the
+  // caller's host copies of the indexes (when given for every problem and the
+  // launch has at most kMaxBoundWgs workgroups): read with the other
+  // arguments, by block index alone, so the first entry loads wait for no
+  // other load
+  int32_t has_bounds;
+  uint32_t wg_bounds[2 * kMaxBoundWgs];
 };
+
+// Barrier for data exchanged through LDS only: waits for this wave's LDS
+// operations, not for its global loads and atomics (a __syncthreads fence
+// would wait for those too, here the entry prefetch and the ticket).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt left at their maximum
+  __builtin_amdgcn_s_barrier();
+}
 
 __device__ __forceinline__ uint4 ld_lds16(uint32_t byte_addr) {
   typedef __attribute__((address_space(3))) const u32x4_t lds_v4_t;
@@ -216,8 +226,10 @@ __device__ __forceinline__ uint4 ld_lds16(uint32_t byte_addr) {
 template <int K, bool XLDS>
 __global__ __launch_bounds__(kSThreads) void k_gemv_sorted(const SortedBatch bt) {
   extern __shared__ uint4 lds[];
+  // (fixed argument offsets: these loads go out together)
   int pi = 0;
-  while (pi + 1 < bt.count && (int)blockIdx.x >= bt.p[pi + 1].wg_begin) ++pi;
+#pragma unroll
+  for (int q = 1; q < kMaxProblems; ++q) pi += (q < bt.count && (int)blockIdx.x >= bt.p[q].wg_begin) ? 1 : 0;
   const SortedProblem& a = bt.p[pi];
   const int local = (int)blockIdx.x - a.wg_begin;
   const int c = local % K;
@@ -237,12 +249,6 @@ __global__ __launch_bounds__(kSThreads) void k_gemv_sorted(const SortedBatch bt)
   uint32_t* idx = reinterpret_cast<uint32_t*>(blk + nslot);
   uint32_t* ticket_lds = idx + bt.bpr + 1;
 
-  // the ticket is taken first; its value is needed only at the end
-  uint32_t ticket = 0;
-  if (threadIdx.x == 0)
-    ticket = __hip_atomic_fetch_add(bt.counters + a.range_begin + r, kTicket / (uint32_t)K, __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_SYSTEM);
-
   const __amdgpu_buffer_rsrc_t rs_e =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(a.entries), (short)0, (int)a.entry_bytes, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t rs_x = __builtin_amdgcn_make_buffer_rsrc(
@@ -250,10 +256,9 @@ __global__ __launch_bounds__(kSThreads) void k_gemv_sorted(const SortedBatch bt)
 
   // The range's steps [S0, S1) are split evenly over the waves.
   uint32_t S0, S1;
-  if (a.bounds_at >= 0) {
-    const int at = a.bounds_at + c * (a.R + 1) + r;
-    S0 = min(bt.bounds[at], a.total_steps);
-    S1 = max(min(bt.bounds[at + 1], a.total_steps), S0);
+  if (bt.has_bounds) {
+    S0 = min(bt.wg_bounds[2 * blockIdx.x], a.total_steps);
+    S1 = max(min(bt.wg_bounds[2 * blockIdx.x + 1], a.total_steps), S0);
   } else {
     S0 = min((uint32_t)__builtin_amdgcn_readfirstlane(gidx[0]), a.total_steps);
     S1 = max(min((uint32_t)__builtin_amdgcn_readfirstlane(gidx[nblk]), a.total_steps), S0);
@@ -271,6 +276,7 @@ __global__ __launch_bounds__(kSThreads) void k_gemv_sorted(const SortedBatch bt)
   };
   uint32_t eA[kSChunk], eB[kSChunk];
   uint32_t s = w_lo;
+  uint32_t ticket;  // (thread 0 only)
 
   // stage the chunk (+ zero codeword), x (+ zero slice) and the range's
   // index; the wave's first entries are loaded at the same time
@@ -304,13 +310,23 @@ __global__ __launch_bounds__(kSThreads) void k_gemv_sorted(const SortedBatch bt)
     }
     if (tid <= nblk) idx[tid] = min(max(iv, S0), S1);
     for (int q = tid; q < nslot; q += kSThreads) blk[q] = -1;
+    // the ticket goes out after the staging and entry loads; its value is
+    // read only after the main loop
+    if (tid == 0)
+      ticket = __hip_atomic_fetch_add(bt.counters + a.range_begin + r, kTicket / (uint32_t)K, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_SYSTEM);
   }
-  __syncthreads();
+  lds_barrier();
 
   float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
   // block (local) of step s and the end of its list
+  // (the blocks after the first whose lists start at or before s, counted
+  // 64 at a time)
   int b = 0;
-  while (b + 1 < nblk && idx[b + 1] <= s) ++b;
+  for (int k0 = 1; k0 < nblk; k0 += kWave) {
+    const int k = k0 + lane;
+    b += __builtin_popcountll(__ballot(k < nblk && idx[min(k, nblk)] <= s));
+  }
   uint32_t bend = idx[b + 1];
   auto flush = [&]() {
     float v = (a0 + a1) + (a2 + a3);
@@ -371,7 +387,7 @@ __global__ __launch_bounds__(kSThreads) void k_gemv_sorted(const SortedBatch bt)
     flush();
   }
   if (threadIdx.x == 0) *ticket_lds = ticket;
-  __syncthreads();
+  lds_barrier();
 
   // rows of the range: add each block's segments in slot order
   // tag: the counter's index and this launch's count on it (never 0, the
@@ -384,13 +400,23 @@ __global__ __launch_bounds__(kSThreads) void k_gemv_sorted(const SortedBatch bt)
   const int rows = min(b_hi * 16, a.d_out) - row0;
   for (int i = (int)threadIdx.x; i < rows; i += kSThreads) {
     const int bi = i >> 4, ri = i & 15;
+    // the block's segments sit in slots bi .. bi + 15, in wave order: all 32
+    // LDS reads go out together, then the matching ones are added in order
+    int bq[kSWaves];
+    float sq[kSWaves];
+#pragma unroll
+    for (int k = 0; k < kSWaves; ++k) {
+      bq[k] = blk[bi + k];
+      sq[k] = seg[(bi + k) * 16 + ri];
+    }
     float v = 0.f;
     bool any = false;
-    for (int q = bi; q < bi + kSWaves; ++q)
-      if (blk[q] == bi) {
-        v = any ? v + seg[q * 16 + ri] : seg[q * 16 + ri];
-        any = true;
-      }
+#pragma unroll
+    for (int k = 0; k < kSWaves; ++k) {
+      const bool m = bq[k] == bi;
+      v = m ? (any ? v + sq[k] : sq[k]) : v;
+      any = any || m;
+    }
     uint64_t* __restrict__ slot = a.part + row0 + i;
     if (!summer) {
       __hip_atomic_store(slot + (size_t)c * a.d_out, (uint64_t)__builtin_bit_cast(uint32_t, v) | ((uint64_t)tag << 32),
@@ -514,22 +540,19 @@ hipError_t launch_gemv_sorted(const SortedLayer* Ls, const uint16_t* const* xs, 
     ranges += R[i];
   }
   if (ranges > (int32_t)(kSortedCounterBytes / 4)) return hipErrorInvalidValue;  // (refused by the caller)
-  // range bounds from the host copies of the indexes, where given and where
-  // they fit the argument block
-  int32_t nbounds = 0;
-  for (int i = 0; i < count; ++i) {
-    SortedProblem& p = bt.p[i];
-    p.bounds_at = -1;
-    const int32_t need = K * (p.R + 1);
-    if (Ls[i].index_host == nullptr || nbounds + need > kMaxBounds) continue;
-    p.bounds_at = nbounds;
-    for (int c = 0; c < K; ++c)
-      for (int r = 0; r <= p.R; ++r) {
-        const int64_t b = (int64_t)r * p.nb / p.R;
-        bt.bounds[nbounds + c * (p.R + 1) + r] = Ls[i].index_host[(size_t)c * p.nb + b];
+  // every workgroup's steps from the host copies of the indexes
+  bt.has_bounds = wgs <= kMaxBoundWgs;
+  for (int i = 0; i < count; ++i) bt.has_bounds = bt.has_bounds && Ls[i].index_host != nullptr;
+  if (bt.has_bounds)
+    for (int i = 0; i < count; ++i) {
+      const SortedProblem& p = bt.p[i];
+      for (int w = 0; w < K * p.R; ++w) {
+        const int c = w % K, r = w / K;
+        const int64_t b0 = (int64_t)r * p.nb / p.R, b1 = (int64_t)(r + 1) * p.nb / p.R;
+        bt.wg_bounds[2 * (p.wg_begin + w)] = Ls[i].index_host[(size_t)c * p.nb + b0];
+        bt.wg_bounds[2 * (p.wg_begin + w) + 1] = Ls[i].index_host[(size_t)c * p.nb + b1];
       }
-    nbounds += need;
-  }
+    }
   bt.bpr = bpr;
   const uint32_t x_bytes = ((uint32_t)G_max + 1u) * 16u;
   const uint32_t tail = (uint32_t)(bpr + kSWaves) * (16u * 4u + 4u) + (uint32_t)(bpr + 1) * 4u + 16u;
