@@ -681,7 +681,7 @@ def persistent_step_row(layers, graph, aq, torch, steps, step_bytes, graph_ms):
             "levels": len(levels), "launches": 1, "vs_graph": graph_ms / ms, "bit_identical_to_graph": same}
 
 
-def sorted_step_row(layers, aq, torch, steps, step_bytes, graph_ms):
+def sorted_step_row(layers, aq, torch, steps, step_bytes, graph_ms, markers=False):
     """The 1x16 decode step over chunk-sorted codes (aqlm_gemv_sorted):
     grouped q/k/v, o, grouped gate/up, down, as one graph; outputs compared
     with the row-major graph's (relative L2)."""
@@ -705,7 +705,7 @@ def sorted_step_row(layers, aq, torch, steps, step_bytes, graph_ms):
     torch.cuda.synchronize()
     err = max(float(torch.linalg.norm((L.y.float() - r.float())) / max(float(torch.linalg.norm(r.float())), 1e-30))
               for L, r in zip(layers, ref))
-    ms = time_steps(g.replay, steps, 2)
+    ms = time_steps(g.replay, steps, 2, markers=markers)
     del g, srt, ref
     return {"ms_per_step": ms, "GBs": step_bytes / (ms * 1e6), "frac": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
             "tok_s_eq": 1000.0 / ms, "launches": len(launches), "vs_row_major_graph": graph_ms / ms,
@@ -763,7 +763,7 @@ def main():
             sys.exit("bench.py: --sorted needs a workload with 15- or 16-bit codes (llama2-7b-1x16)")
         layers, launches, graph, ms, spread, step_bytes = decode_step(model, M, B, step_seed(M), aq, args.steps,
                                                                       args.warmup)
-        row = sorted_step_row(layers, aq, torch, args.steps, step_bytes, ms)
+        row = sorted_step_row(layers, aq, torch, args.steps, step_bytes, ms, markers=True)
         print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "sorted_codes": row}), flush=True)
         return
     layers, launches, graph, ms, spread, step_bytes = decode_step(
