@@ -29,6 +29,7 @@
 // bit-reproducible from run to run.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 
 namespace aqlm {
 
@@ -129,9 +130,9 @@ __global__ __launch_bounds__(kBwThreads) void k_grad_cb(const BwArgs a) {
       cv = *reinterpret_cast<const uint4*>(a.codes + ((size_t)i * G + j0) * M + 16 * q);
     }
     if (tid < kBwT && i0 + tid < a.d_out) scv = h2f(a.scales[i0 + tid]);
-    __syncthreads();  // (the previous tile's last reads of stage 0 and of the tile's codes are done)
+    lds_barrier();  // (the previous tile's last reads of stage 0 and of the tile's codes are done)
     store(0, vd, vx);
-    __syncthreads();
+    lds_barrier();
     for (int step = 0; step < nsteps; ++step) {
       const bool more = step + 1 < nsteps;
       if (more) load(step + 1, i0, c0, vd, vx);
@@ -149,7 +150,7 @@ __global__ __launch_bounds__(kBwThreads) void k_grad_cb(const BwArgs a) {
         for (int nj = 0; nj < 2; ++nj)
           acc[mi][nj] = __builtin_amdgcn_mfma_f32_16x16x32_f16(af[mi], bf[nj], acc[mi][nj], 0, 0, 0);
       if (more) store((step + 1) & 1, vd, vx);
-      __syncthreads();
+      lds_barrier();
     }
     if (vec_codes) {
       if (tid < kCodeU4) reinterpret_cast<uint4*>(tcodes)[tid] = cv;
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(kBwThreads) void k_grad_cb(const BwArgs a) {
       }
     }
     if (tid < kBwT) tscales[tid] = scv;
-    __syncthreads();
+    lds_barrier();
 
     // Scatter: lane holds G[i][c] for i = i0 + 64 wm + 16 mi + 4 slot + r and
     // c = c0 + 32 wn + 16 nj + r16.
@@ -207,7 +208,7 @@ __global__ __launch_bounds__(kBwThreads) void k_grad_cb(const BwArgs a) {
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   for (int e = tid; e < M * 2048; e += kBwThreads) {
     const float v = dcl[e];
     if (v != 0.f) atomicAdd(&a.dcb[e], v);

@@ -10,6 +10,7 @@
 // read their codebooks (up to 2 x 1 MiB) through L2.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 
 namespace aqlm {
 
@@ -78,7 +79,7 @@ __global__ __launch_bounds__(256) void k_dequant(const void* __restrict__ codes,
   __shared__ uint4 cb_lds[kLdsEntries];
   if constexpr (B == 8) {
     for (int e = threadIdx.x; e < M * 256; e += 256) cb_lds[e] = cb[e];
-    __syncthreads();
+    lds_barrier();
   }
   const uint32_t stride = gridDim.x * 256u;
   for (uint32_t q = blockIdx.x * 256u + threadIdx.x; q < total_groups; q += stride) {

@@ -16,6 +16,7 @@
 // bank quads without padding.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 
 namespace aqlm {
 
@@ -151,7 +152,7 @@ __global__ __launch_bounds__(WM * WN * kWave) void k_gemm_f16(const GemmF16Args 
     compute(k);
     if (k + 1 < ksteps) l_store(k + 1, next);
     g_load(k + 1 + kDepth, next);
-    __syncthreads();
+    lds_barrier();  // (the loads just issued stay in flight)
   };
   if constexpr (kDepth == 3) {
     g_load(0, IntC<0>{});

@@ -21,6 +21,7 @@
 // formats with M in {1, 2}.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 
 namespace aqlm {
 
@@ -140,7 +141,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
     for (int nb = 0; nb < NB; ++nb) acc[rb][nb] = f4_t{0.f, 0.f, 0.f, 0.f};
 
   for (int32_t it = 0; it < iters; ++it) {
-    __syncthreads();  // previous x tiles fully read
+    lds_barrier();  // previous x tiles fully read
     // Stage the x tiles of K-tiles it*KSPLIT .. it*KSPLIT+KSPLIT-1.
     for (int e = tid; e < KSPLIT * kTok * C::kGT; e += kThreads) {
       const int ks = e / (kTok * C::kGT);
@@ -153,7 +154,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
       if (tok < n && grp < G) v = x[(int64_t)tok * G + grp];
       x_lds[ks * kXTile + t * kPitch + jl] = v;
     }
-    __syncthreads();
+    lds_barrier();
 
     const int32_t kt = it * KSPLIT + kl;
     uint32_t cur[RB][C::kWords];
@@ -203,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
   if constexpr (KSPLIT > 1) {
     // Waves kl = 1..KSPLIT-1 hand their partial sums to wave kl = 0 of the
     // same row group, which adds them in ascending kl.
-    __syncthreads();
+    lds_barrier();
     f4_t* red = reinterpret_cast<f4_t*>(x_lds);
     if (kl > 0) {
 #pragma unroll
@@ -212,7 +213,7 @@ __global__ __launch_bounds__(kThreads) void k_gemm_mfma(const uint8_t* __restric
         for (int nb = 0; nb < NB; ++nb)
           red[(((kl - 1) * kRowGroups + rgrp) * RB * NB + rb * NB + nb) * kWave + lane] = acc[rb][nb];
     }
-    __syncthreads();
+    lds_barrier();
     if (kl != 0) return;
 #pragma unroll
     for (int k = 1; k < KSPLIT; ++k)

@@ -19,6 +19,7 @@
 // per row block, so results are deterministic.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 #include "stream_common.h"
 
 namespace aqlm {
@@ -159,14 +160,14 @@ __global__ __launch_bounds__(kThreadsNB) void k_gemm_nb(const GemmNbArgs a) {
     for (int d = 0; d < D; ++d) {
       const int j = j0 + d;
       if (j < R) {
-        if (j > 0) __syncthreads();  // round j - 1's x fully read
+        if (j > 0) lds_barrier();  // round j - 1's x fully read
 #pragma unroll
         for (int i = 0; i < N::kXV; ++i) {
           const int e = tid + i * kThreadsNB;
           if (e < n * kXG) x_lds[e] = xv[i];
         }
         if (j + 1 < R) load_x(j + 1);
-        __syncthreads();
+        lds_barrier();
       }
       const bool live = j < nks;
       if (live) {
@@ -220,10 +221,10 @@ __global__ __launch_bounds__(kThreadsNB) void k_gemm_nb(const GemmNbArgs a) {
   // 4 * slot + i), then (row, token) threads add the 16 waves in order.
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    __syncthreads();  // previous block's sums read (and the last round's x)
+    lds_barrier();  // previous block's sums read (and the last round's x)
 #pragma unroll
     for (int i = 0; i < 4; ++i) part[(wave * 16 + 4 * slot + i) * 16 + r16] = acc[rb][i];
-    __syncthreads();
+    lds_barrier();
     if (tid < 16 * n) {
       const int rr = tid & 15, t = tid >> 4;
       float s = 0.f;

@@ -19,6 +19,7 @@
 // lane gathers its codewords with 16-byte global loads.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 
 namespace aqlm {
 
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(THREADS) void k_gemv(const uint8_t* __restrict__ co
       for (int k = 0; k < C::kCopies; ++k) cb_lds[e * C::kCopies + ((k + lane) % C::kCopies)] = v;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   const uint32_t copy_off = (B == 8) ? (uint32_t)(lane % (C::kCopies ? C::kCopies : 1)) * 16u : 0u;
   if (nr > 0) {
@@ -175,7 +176,7 @@ __global__ __launch_bounds__(THREADS) void k_gemv(const uint8_t* __restrict__ co
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   for (int t = tid; t < rows_local; t += THREADS) {
     float s = 0.f;
     for (int c = 0; c < nchunks; ++c) s += part[t * nchunks + c];

@@ -46,6 +46,7 @@
 // counts exactly the loads issued after the one it needs.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 
 namespace aqlm {
 
@@ -158,7 +159,7 @@ __global__ __launch_bounds__(kLThreads) void k_gemv_lut(const GemvBatch bt) {
   for (int u = 0; u < Q; ++u) acc[u] = 0.f;
 
   build(0, xr[0]);
-  __syncthreads();
+  lds_barrier();
 
   // 3. K-slices, D per trip: slice ks = j0 + d uses ring slot d and table
   // buffer d & 1; it builds slice ks + 1's table into the other buffer and
@@ -189,7 +190,7 @@ __global__ __launch_bounds__(kLThreads) void k_gemv_lut(const GemvBatch bt) {
         for (int u = 0; u < Q; ++u)
           if (u < nq) acc[u] += (tv[u][0] + tv[u][1]) + (tv[u][2] + tv[u][3]);
         issue(ks + D, xr[d], ring[d]);
-        __syncthreads();
+        lds_barrier();
       }
     }
   }

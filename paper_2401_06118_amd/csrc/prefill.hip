@@ -23,6 +23,7 @@
 // ahead of their use.
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 
 namespace aqlm {
 
@@ -276,17 +277,17 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
     };
     p_load(0, IntC<0>{});
     p_load(1, IntC<1>{});
-    __syncthreads();  // codebook copies visible
+    lds_barrier();  // codebook copies visible
     if constexpr (B > 8) p_gather(IntC<0>{});
     p_store(0, IntC<0>{});
     p_load(2, IntC<0>{});
     if constexpr (B > 8) p_gather(IntC<1>{});
-    __syncthreads();
+    lds_barrier();
     for (int k = 0; k < ksteps; k += 2) {
       p_step(k, IntC<1>{}, IntC<0>{});
-      __syncthreads();
+      lds_barrier();
       p_step(k + 1, IntC<0>{}, IntC<1>{});
-      if (k + 1 < ksteps) __syncthreads();  // the consumers pass one barrier per step
+      if (k + 1 < ksteps) lds_barrier();  // the consumers pass one barrier per step
     }
   } else {
     // Wave c owns tokens BN / 2 * (c % 2) .. (kTB blocks) and rows
@@ -298,8 +299,8 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
     for (int tb = 0; tb < kTB; ++tb)
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb) acc[tb][rb] = f4_t{0.f, 0.f, 0.f, 0.f};
-    __syncthreads();
-    __syncthreads();
+    lds_barrier();
+    lds_barrier();
     for (int k = 0; k < ksteps; ++k) {
       const uint4* at = a_lds + (k & 1) * kATileU4;
       const uint4* xt = x_lds + (k & 1) * kXTileU4;
@@ -318,7 +319,7 @@ __global__ __launch_bounds__(kPfThreads) void k_prefill(const PrefillArgs a, int
             acc[tb][rb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(xf, wf[rb], acc[tb][rb], 0, 0, 0);
         }
       }
-      __syncthreads();
+      lds_barrier();
     }
 
     // D[token][row]: lane holds row r16 of its block and tokens 4 * slot + i.

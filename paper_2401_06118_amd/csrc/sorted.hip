@@ -30,6 +30,7 @@
 
 #include "common.h"
 #include "launch.h"
+#include "lds_sync.h"
 #include "sorted.h"
 
 namespace aqlm {
@@ -195,14 +196,6 @@ struct SortedBatch {
   int32_t has_bounds;
   uint32_t wg_bounds[2 * kMaxBoundWgs];
 };
-
-// Barrier for data exchanged through LDS only: waits for this wave's LDS
-// operations, not for its global loads and atomics (a __syncthreads fence
-// would wait for those too, here the entry prefetch and the ticket).
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt left at their maximum
-  __builtin_amdgcn_s_barrier();
-}
 
 __device__ __forceinline__ uint4 ld_lds16(uint32_t byte_addr) {
   typedef __attribute__((address_space(3))) const u32x4_t lds_v4_t;
