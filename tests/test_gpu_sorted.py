@@ -230,3 +230,23 @@ def test_gemv_sorted_without_host_index_same_bits():
         assert st == 0
         torch.cuda.synchronize()
         assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+@pytest.mark.parametrize("d_out,d_in", [(1, 2048), (16, 8), (210_000, 64)])
+def test_gemv_sorted_extreme_shapes(d_out, d_in):
+    """One row; one block of one group; and a layer tall enough to need more
+    row ranges than one workgroup round holds (13125 blocks: 33 ranges of at
+    most 400 blocks, 264 workgroups on 256 CUs, so the workgroups' step
+    ranges come from the device index and the summing workgroups poll
+    partners that run in the same round or an earlier one)."""
+    print(f"[sorted extreme] {d_out}x{d_in}", flush=True)
+    lay = synth.layer(33_000 + d_out + d_in, d_out, d_in, 1, 16)
+    codes, cb, sc, x = to_device(lay)
+    y = aq().SortedCodes(codes, cb, sc).gemv(x[0])
+    torch.cuda.synchronize()
+    if d_out <= 4096:
+        check(lay, fp16_to_np(y))
+    else:
+        rows = np.sort(np.random.default_rng(d_out).choice(d_out, size=200, replace=False))
+        rows = np.unique(np.concatenate([rows, [0, 6399, 6400, d_out - 1]]))
+        check(lay, fp16_to_np(y), rows)
