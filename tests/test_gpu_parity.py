@@ -358,6 +358,30 @@ def test_gemm_workspace_prefill_layer_sampled_rows(n, M, B):
     check_products(lay, y, rows)
 
 
+@pytest.mark.parametrize("d_out,d_in,M,B,n", [
+    (11000, 1024, 4, 8, 500),   # 128 x 256 tiles, ragged tokens and rows
+    (11000, 64, 2, 8, 500),     # 128 x 256 tiles, one K-step (fewer steps than stages)
+    (11000, 576, 2, 8, 1000),   # 256 x 192 tiles
+    (8000, 512, 1, 16, 2000),   # 256 x 256 tiles
+    (8100, 192, 2, 8, 1900),    # 256 x 256 tiles, three K-steps
+    (11000, 64, 4, 8, 1030),    # 256 x 256 tiles, one K-step
+])
+def test_gemm_workspace_tile_shapes(d_out, d_in, M, B, n):
+    """The dense product's larger tile shapes (chosen by tile count on a
+    256-CU GPU), with ragged edges: every token against the oracle on sampled
+    rows around the tile boundaries, and a second call bit for bit."""
+    print(f"[gemm-ws tiles] {d_out}x{d_in} M={M} B={B} n={n}", flush=True)
+    lay = synth.layer(8400 + d_out + d_in + n, d_out, d_in, M, B, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y1 = aq().gemm(codes, cb, sc, x)
+    y2 = aq().gemm(codes, cb, sc, x)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+    edges = [0, 127, 128, 191, 192, 255, 256, d_out - 257, d_out - 256, d_out - 1]
+    rows = np.unique(np.concatenate([edges, np.random.default_rng(d_out + n).integers(0, d_out, 30)]))
+    check_products(lay, fp16_to_np(y1), rows)
+
+
 @pytest.mark.parametrize("d_out,d_in,M,B,n", [(300, 1040, 2, 8, 63), (300, 1040, 4, 8, 200), (200, 1024, 2, 8, 16)])
 def test_gemm_without_workspace_is_small_batch(d_out, d_in, M, B, n):
     """When the size query says 0 the call is exactly aqlm_gemm_small_batch
