@@ -96,6 +96,9 @@ def parse_args():
                     help="only time the Phase-1 beam search (aqlm_beam_search) and exit")
     ap.add_argument("--once", action="store_true",
                     help="with --compare-paths: launch each family once per case, untimed (for counter runs)")
+    ap.add_argument("--floors", action="store_true",
+                    help="only run the microbenchmarks of the GPU's limits (launch, dependent load, HBM read "
+                         "stream, matrix-core issue rate, LDS and L2 gathers) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy a few times (the reference kernel for "
                          "scaling HBM byte counters) and exit")
@@ -645,6 +648,76 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": COPY_BYTES, "launches": 5}), flush=True)
 
 
+CLOCK_GHZ = 2.4  # MI355X peak engine clock
+
+
+def floors(torch):
+    """Microbenchmarks of the limits the kernels are measured against
+    (paper_2401_06118_amd/floors/floors.hip, a library of its own), each a
+    HIP graph of back-to-back launches timed with an event pair; per-clock
+    figures assume the 2.4 GHz peak clock."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2401_06118_amd",
+                                   "libaqlm_floors.so"))
+    vp, ci, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    lib.floor_empty.argtypes = [ci, vp]
+    lib.floor_dep_load.argtypes = [vp, vp, ci, vp]
+    lib.floor_read.argtypes = [vp, sz, vp, ci, vp]
+    lib.floor_mfma.argtypes = [vp, ci, ci, vp]
+    lib.floor_lds_gather.argtypes = [vp, ci, ci, ci, vp]
+    lib.floor_l2_gather.argtypes = [vp, ctypes.c_uint32, vp, ci, ci, vp]
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    stream = lambda: torch.cuda.current_stream().cuda_stream  # noqa: E731
+
+    def ok(st):
+        if st != 0:
+            raise RuntimeError(f"floor launch failed: hipError {st}")
+
+    def per_launch_ms(call, reps, steps=5):
+        g = graph_of([call] * reps)
+        ms = time_steps(g.replay, steps=steps, warmup=2) / reps
+        del g
+        return ms
+
+    rows = []
+    ms = per_launch_ms(lambda: ok(lib.floor_empty(cus, stream())), 200)
+    rows.append({"floor": "empty launch", "workgroups": cus, "threads": 1024, "us": ms * 1e3})
+    src = torch.ones(cus * 64, dtype=torch.int32, device="cuda")
+    dst = torch.empty(cus * 1024, dtype=torch.int32, device="cuda")
+    ms = per_launch_ms(lambda: ok(lib.floor_dep_load(src.data_ptr(), dst.data_ptr(), cus, stream())), 200)
+    rows.append({"floor": "one dependent load (line in L2), barrier, store", "workgroups": cus, "threads": 1024,
+                 "us": ms * 1e3})
+    del src, dst
+    buf = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
+    out = torch.empty(cus * 16 * 256, dtype=torch.int32, device="cuda")
+    ms = per_launch_ms(lambda: ok(lib.floor_read(buf.data_ptr(), (1 << 30) // 16, out.data_ptr(), cus * 16,
+                                                 stream())), 10)
+    rows.append({"floor": "HBM read stream, 1 GiB", "GBs": (1 << 30) / (ms * 1e6)})
+    del buf, out
+    iters = 2000
+    out = torch.empty(cus * 4 * 256, dtype=torch.float32, device="cuda")
+    ms = per_launch_ms(lambda: ok(lib.floor_mfma(out.data_ptr(), cus * 4, iters, stream())), 3)
+    mfmas = cus * 4 * 4 * iters * 8
+    rows.append({"floor": "v_mfma_f32_16x16x32_f16, 4 waves per SIMD, 8 chains each",
+                 "clocks_per_mfma_per_simd": ms * 1e-3 * CLOCK_GHZ * 1e9 * cus * 4 / mfmas,
+                 "TFLOPs": mfmas * 16 * 16 * 32 * 2 / (ms * 1e9)})
+    del out
+    out = torch.empty(cus * 1024, dtype=torch.int32, device="cuda")
+    for copies in (1, 8, 16):
+        iters = 500
+        ms = per_launch_ms(lambda: ok(lib.floor_lds_gather(out.data_ptr(), cus, iters, copies, stream())), 3)
+        nbytes = cus * 1024 * iters * 8 * 16
+        rows.append({"floor": f"LDS 16-byte gathers, {copies} table copies", "bytes_per_clock_per_cu":
+                     nbytes / (ms * 1e-3 * CLOCK_GHZ * 1e9 * cus)})
+    tab = torch.ones(1 << 20, dtype=torch.uint8, device="cuda")
+    iters = 50
+    ms = per_launch_ms(lambda: ok(lib.floor_l2_gather(tab.data_ptr(), (1 << 20) // 16, out.data_ptr(), cus, iters,
+                                                      stream())), 3)
+    rows.append({"floor": "16-byte gathers from a 1 MiB table in L2", "gathers_per_clock_per_cu":
+                 cus * 1024 * iters * 8 / (ms * 1e-3 * CLOCK_GHZ * 1e9 * cus)})
+    return rows
+
+
 def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False):
     """Build a decode step, capture it as one graph and time its replays."""
     layers = decode_step_layers(model, M, B, seed0)
@@ -730,6 +803,9 @@ def main():
         copy_calibration()
         return
     import torch
+    if args.floors:
+        print(json.dumps({"floors": floors(torch)}), flush=True)
+        return
     import paper_2401_06118_amd as aq
     from paper_2401_06118_amd import _lib
 

@@ -17,6 +17,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libaqlm_mi355x.so")
+# Measurement-only microbenchmarks (bench.py --floors), a library of their own.
+FLOORS_SRC = os.path.join(HERE, "floors", "floors.hip")
+FLOORS_LIB = os.path.join(HERE, "libaqlm_floors.so")
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -58,6 +61,14 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    tmp = FLOORS_LIB + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-shared", "-o", tmp, FLOORS_SRC]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {FLOORS_SRC}:\n{r.stdout}{r.stderr}")
+    os.replace(tmp, FLOORS_LIB)
     return LIB
 
 

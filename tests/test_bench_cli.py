@@ -36,3 +36,30 @@ def test_trace_summary_keeps_only_the_marked_region(tmp_path):
     a = out["kernels"]["aqlm::k_a"]
     assert a["calls"] == 2 and a["total_us"] == 22.0 and a["avg_us"] == 11.0
     assert out["kernels"]["aqlm::k_b"]["calls"] == 1
+
+
+def test_floors_library_exports_and_refuses_bad_arguments():
+    """The measurement library behind bench.py --floors is built beside the
+    product library, exports its six microbenchmarks, and refuses arguments
+    that would put an access out of range before any launch (so no GPU is
+    needed here)."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2401_06118_amd", "libaqlm_floors.so")
+    if not os.path.exists(path):
+        import pytest
+        pytest.skip("libraries not built (python -m paper_2401_06118_amd.build)")
+    lib = ctypes.CDLL(path)
+    names = ["floor_empty", "floor_dep_load", "floor_read", "floor_mfma", "floor_lds_gather", "floor_l2_gather"]
+    for n in names:
+        assert hasattr(lib, n), n
+    vp, ci = ctypes.c_void_p, ctypes.c_int
+    lib.floor_lds_gather.argtypes = [vp, ci, ci, ci, vp]
+    lib.floor_l2_gather.argtypes = [vp, ctypes.c_uint32, vp, ci, ci, vp]
+    lib.floor_read.argtypes = [vp, ctypes.c_size_t, vp, ci, vp]
+    invalid = 1  # hipErrorInvalidValue
+    fake = 0x10000
+    assert lib.floor_lds_gather(fake, 1, 1, 17, None) == invalid   # more copies than the table holds
+    assert lib.floor_lds_gather(fake, 1, 1, 0, None) == invalid
+    assert lib.floor_l2_gather(fake, 3000, fake, 1, 1, None) == invalid  # not a power of two
+    assert lib.floor_read(fake, 0, fake, 1, None) == invalid
+    assert lib.floor_read(None, 16, fake, 1, None) == invalid
