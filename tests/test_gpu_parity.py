@@ -80,7 +80,7 @@ def test_dequantize_bit_exact(d_out, d_in, M, B):
     assert_bits_equal(dequant_gpu(lay), oracle.dequantize(lay.codes, lay.codebooks, lay.scales), "dequantize")
 
 
-@pytest.mark.parametrize("M,B", [(1, 8), (2, 8), (3, 8), (4, 8), (8, 8), (1, 16)])
+@pytest.mark.parametrize("M,B", [(1, 8), (2, 8), (3, 8), (4, 8), (8, 8), (1, 16), (2, 12)])
 def test_dequantize_special_values_bit_exact(M, B):
     """Codebooks and scales mixing random finite fp16 patterns with signed
     zeros, subnormals, ties and values whose scaled sums overflow."""
