@@ -348,10 +348,8 @@ hipError_t run_gemm_f16(const uint16_t* x, const uint16_t* w, uint16_t* y, float
 
 bool gemm_f16_supported(int32_t d_in) { return d_in % kGfK == 0; }
 
-int32_t gemm_f16_splits(int64_t n, int64_t d_out, int64_t K) { return gf_splits(gf_choose(n, d_out), n, d_out, K); }
-
 size_t gemm_f16_part_bytes(int64_t n, int64_t d_out, int64_t K) {
-  const int32_t s = gemm_f16_splits(n, d_out, K);
+  const int32_t s = gf_splits(gf_choose(n, d_out), n, d_out, K);
   return s > 1 ? (size_t)s * (size_t)n * (size_t)d_out * sizeof(float) : 0;
 }
 
