@@ -959,6 +959,8 @@ def main():
         log("backward done")
         sec["beam_search"] = beam_rows(aq, torch)
         log("beam search done")
+        sec["floors"] = floors(torch)
+        log("floors done")
         result["secondary"] = sec
     if not args.no_cpu_baseline:
         layers = decode_step_layers(model, M, B, step_seed(M))
