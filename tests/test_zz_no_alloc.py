@@ -39,6 +39,7 @@ def with_workspace(lay_dev):
 @pytest.mark.parametrize("first,second", [
     ((11008, 4096, 4, 8, 256), (1000, 2048, 2, 8, 100)),   # 86 MiB of weights, then a small product
     ((4096, 11008, 1, 16, 64), (300, 1024, 4, 8, 64)),    # split along d_in (fp32 partials), then smaller
+    ((11000, 576, 2, 8, 1000), (8000, 512, 1, 16, 2000)),  # the dense product's 256-token tiles, fewer weights second
 ])
 def test_noalloc_matches_workspace_product_twice(lib, first, second):
     for k, (d_out, d_in, M, B, n) in enumerate((first, second)):
