@@ -673,30 +673,30 @@ def floors(torch):
         if st != 0:
             raise RuntimeError(f"floor launch failed: hipError {st}")
 
-    def per_launch_ms(call, reps, steps=5):
+    def graph_launch_ms(call, reps, steps=5):
         g = graph_of([call] * reps)
         ms = time_steps(g.replay, steps=steps, warmup=2) / reps
         del g
         return ms
 
     rows = []
-    ms = per_launch_ms(lambda: ok(lib.floor_empty(cus, stream())), 200)
+    ms = graph_launch_ms(lambda: ok(lib.floor_empty(cus, stream())), 200)
     rows.append({"floor": "empty launch", "workgroups": cus, "threads": 1024, "us": ms * 1e3})
     src = torch.ones(cus * 64, dtype=torch.int32, device="cuda")
     dst = torch.empty(cus * 1024, dtype=torch.int32, device="cuda")
-    ms = per_launch_ms(lambda: ok(lib.floor_dep_load(src.data_ptr(), dst.data_ptr(), cus, stream())), 200)
+    ms = graph_launch_ms(lambda: ok(lib.floor_dep_load(src.data_ptr(), dst.data_ptr(), cus, stream())), 200)
     rows.append({"floor": "one dependent load (line in L2), barrier, store", "workgroups": cus, "threads": 1024,
                  "us": ms * 1e3})
     del src, dst
     buf = torch.ones(1 << 30, dtype=torch.uint8, device="cuda")
     out = torch.empty(cus * 16 * 256, dtype=torch.int32, device="cuda")
-    ms = per_launch_ms(lambda: ok(lib.floor_read(buf.data_ptr(), (1 << 30) // 16, out.data_ptr(), cus * 16,
+    ms = graph_launch_ms(lambda: ok(lib.floor_read(buf.data_ptr(), (1 << 30) // 16, out.data_ptr(), cus * 16,
                                                  stream())), 10)
     rows.append({"floor": "HBM read stream, 1 GiB", "GBs": (1 << 30) / (ms * 1e6)})
     del buf, out
     iters = 2000
     out = torch.empty(cus * 4 * 256, dtype=torch.float32, device="cuda")
-    ms = per_launch_ms(lambda: ok(lib.floor_mfma(out.data_ptr(), cus * 4, iters, stream())), 3)
+    ms = graph_launch_ms(lambda: ok(lib.floor_mfma(out.data_ptr(), cus * 4, iters, stream())), 3)
     mfmas = cus * 4 * 4 * iters * 8
     rows.append({"floor": "v_mfma_f32_16x16x32_f16, 4 waves per SIMD, 8 chains each",
                  "clocks_per_mfma_per_simd": ms * 1e-3 * CLOCK_GHZ * 1e9 * cus * 4 / mfmas,
@@ -705,13 +705,13 @@ def floors(torch):
     out = torch.empty(cus * 1024, dtype=torch.int32, device="cuda")
     for copies in (1, 8, 16):
         iters = 500
-        ms = per_launch_ms(lambda: ok(lib.floor_lds_gather(out.data_ptr(), cus, iters, copies, stream())), 3)
+        ms = graph_launch_ms(lambda: ok(lib.floor_lds_gather(out.data_ptr(), cus, iters, copies, stream())), 3)
         nbytes = cus * 1024 * iters * 8 * 16
         rows.append({"floor": f"LDS 16-byte gathers, {copies} table copies", "bytes_per_clock_per_cu":
                      nbytes / (ms * 1e-3 * CLOCK_GHZ * 1e9 * cus)})
     tab = torch.ones(1 << 20, dtype=torch.uint8, device="cuda")
     iters = 50
-    ms = per_launch_ms(lambda: ok(lib.floor_l2_gather(tab.data_ptr(), (1 << 20) // 16, out.data_ptr(), cus, iters,
+    ms = graph_launch_ms(lambda: ok(lib.floor_l2_gather(tab.data_ptr(), (1 << 20) // 16, out.data_ptr(), cus, iters,
                                                       stream())), 3)
     rows.append({"floor": "16-byte gathers from a 1 MiB table in L2", "gathers_per_clock_per_cu":
                  cus * 1024 * iters * 8 / (ms * 1e-3 * CLOCK_GHZ * 1e9 * cus)})
