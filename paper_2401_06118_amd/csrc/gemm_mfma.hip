@@ -257,10 +257,11 @@ hipError_t run_shape(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, 
   // Up to 16 tokens: one token block, 16-row workgroups whose four waves split
   // K (many workgroups, like the matrix-vector kernel).  More tokens: 128-row
   // by 64-token tiles, each codeword fragment reused for 4 token blocks.
-  // 2x12 stages 128 KiB of codebooks per workgroup: 64-row workgroups
-  // amortise it (11008x4096, n = 16: 34.8 us, against 59.7 us with 16 rows
-  // and 45.8 us gathering from L2).
-  if (n <= 16 && MfmaCfg<M, B>::kWideLds) return run<M, B, VEC, 4, 1, 4>(L, n, x, y, s);
+  // 2x12 stages 128 KiB of codebooks per workgroup: 48-row workgroups
+  // amortise it and still cover most CUs (11008x4096, n = 4 / 16: 32.0 /
+  // 32.4 us, against 34.2 / 35.0 with 64 rows, 36.7 / 37.6 with 80, 59.7 at
+  // n = 16 with 16 rows and 45.8 gathering from L2).
+  if (n <= 16 && MfmaCfg<M, B>::kWideLds) return run<M, B, VEC, 3, 1, 4>(L, n, x, y, s);
   if (n <= 16) return run<M, B, VEC, 1, 1, 4>(L, n, x, y, s);
   return run<M, B, VEC, 2, 4, 1>(L, n, x, y, s);
 }
