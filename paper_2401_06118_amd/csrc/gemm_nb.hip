@@ -29,7 +29,11 @@ namespace {
 constexpr int kWavesNB = 16;
 constexpr int kThreadsNB = kWavesNB * kWave;
 constexpr int kMaxTokNB = 16;  // tokens per launch (the 16 MFMA columns)
-constexpr int kInFlightNB = 3;
+// code items requested ahead of their use per wave (at least both items of a
+// pair of row blocks); 11008x4096 4x8 at 2 / 4 / 8 / 16 tokens: 12.7 / 14.1
+// / 15.9 / 18.2 us with 2, 13.4 / 14.8 / 16.4 / 18.7 with 3, slower with 4
+// or 6; 2x8 and other shapes the same with 2 or 3
+constexpr int kInFlightNB = 2;
 constexpr size_t kLdsLimit = 160 * 1024;
 
 struct GemmNbArgs {
