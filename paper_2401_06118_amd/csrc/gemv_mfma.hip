@@ -343,12 +343,14 @@ __device__ __forceinline__ bool ks_body(const GemvBatch& bt, const int vwg, Wait
   // consumed in pairs, so a load is used at least kAhead - 2 items after it
   // is requested.
   constexpr int kSlots = D * RB;
-  // Paired blocks: four items ahead, so each load has a whole pair of items
-  // computed between its request and its use.  Measured on the Llama-2
-  // shapes, five or six ahead were slower (more of a workgroup's stream in
-  // flight at once delays the items that every wave needs first).  Single
-  // blocks: the whole ring.
-  constexpr int kAheadWant = RB >= 2 ? 4 : 8;
+  // Paired blocks: two items ahead (the next pair is requested as the
+  // current one starts).  Fewer code loads in flight per wave let the items
+  // that every wave needs next arrive sooner, and 16 waves x 2 items still
+  // keep about 8 MiB in flight across the chip.  Measured (same box):
+  // Llama-2-70B step 5.38-5.41 ms with two ahead, 5.50-5.51 with three,
+  // 5.87-5.90 with four (five or six slower still); 7B step 0.853 / 0.906 /
+  // 0.888 ms.  Single blocks: the whole ring (four ahead measured the same).
+  constexpr int kAheadWant = RB >= 2 ? 2 : 8;
   constexpr int kAhead = kAheadWant < kSlots ? kAheadWant : kSlots;
   static_assert(RB < 2 || kAhead >= 2, "both items of a pair must be requested before the pair starts");
   extern __shared__ uint4 lds[];
