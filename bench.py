@@ -70,6 +70,9 @@ def parse_args():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--spread-steps", type=int, default=20,
+                    help="event-timed replays of the per-step spread pass after the timed region (counter runs "
+                         "use few: every dispatch is serialised under counter collection)")
     ap.add_argument("--workload", default="llama2-70b-2x8", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true")
@@ -718,7 +721,7 @@ def floors(torch):
     return rows
 
 
-def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False):
+def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False, spread_steps=20):
     """Build a decode step, capture it as one graph and time its replays."""
     layers = decode_step_layers(model, M, B, seed0)
     step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
@@ -727,7 +730,7 @@ def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False):
     graph = graph_of(launches)
     log(f"{model} {M}x{B}: graph captured")
     ms = time_steps(graph.replay, steps, warmup, markers=markers)
-    spread = step_spread(graph.replay, max(steps, 20))
+    spread = step_spread(graph.replay, max(1, spread_steps))
     return layers, launches, graph, ms, spread, step_bytes
 
 
@@ -843,7 +846,7 @@ def main():
         print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "sorted_codes": row}), flush=True)
         return
     layers, launches, graph, ms, spread, step_bytes = decode_step(
-        model, M, B, step_seed(M), aq, args.steps, args.warmup, markers=True)
+        model, M, B, step_seed(M), aq, args.steps, args.warmup, markers=True, spread_steps=args.spread_steps)
     log(f"{args.workload}: {len(layers)} layers in {len(launches)} launches, {step_bytes / 1e9:.3f} GB per step; "
         f"step {ms:.4f} ms (graph replay)")
 
