@@ -91,6 +91,8 @@ def parse_args():
                     help="only time the gradients through Eq. 2 (aqlm_backward) and exit")
     ap.add_argument("--persistent", action="store_true",
                     help="only the workload's step as one persistent launch (aqlm_gemv_step) beside its graph")
+    ap.add_argument("--tiled", action="store_true",
+                    help="the decode step over tiled 8-bit codes (aqlm_gemv_grouped_tiled), beside the row-major graph")
     ap.add_argument("--sorted", action="store_true",
                     help="only the workload's step (a 1x16 one) over chunk-sorted codes beside its graph")
     ap.add_argument("--single-layers", action="store_true",
@@ -162,6 +164,16 @@ def launches_by_dependency(layers, aq):
         out.append(lambda o=o: o.gemv(aq))
         out.append(lambda gate=gate, up=up: aq.gemv_grouped([gate.problem(), up.problem()]))
         out.append(lambda down=down: down.gemv(aq))
+    return out
+
+
+def launches_tiled(layers, tiled, aq):
+    """launches_by_dependency over tiled codes (aqlm_gemv_grouped_tiled),
+    writing the same outputs."""
+    out = []
+    for b in range(0, len(layers), 7):
+        grp = lambda idx: (lambda: aq.gemv_tiled_grouped([(tiled[i], layers[i].x[0], layers[i].y[0]) for i in idx]))
+        out += [grp([b, b + 1, b + 2]), grp([b + 3]), grp([b + 4, b + 5]), grp([b + 6])]
     return out
 
 
@@ -721,12 +733,18 @@ def floors(torch):
     return rows
 
 
-def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False, spread_steps=20):
-    """Build a decode step, capture it as one graph and time its replays."""
+def decode_step(model, M, B, seed0, aq, steps, warmup, markers=False, spread_steps=20, tiled=False):
+    """Build a decode step, capture it as one graph and time its replays.
+    tiled: the codes are also stored tiled (aqlm_tile_codes, before anything
+    is timed) and the step runs over those."""
     layers = decode_step_layers(model, M, B, seed0)
     step_bytes = sum(L.shape.gemv_bytes(1) for L in layers)
     log(f"{model} {M}x{B}: {len(layers)} layers built")
-    launches = launches_by_dependency(layers, aq)
+    if tiled:
+        tl = [aq.TiledCodes(L.codes, L.codebooks, L.scales) for L in layers]
+        launches = launches_tiled(layers, tl, aq)
+    else:
+        launches = launches_by_dependency(layers, aq)
     graph = graph_of(launches)
     log(f"{model} {M}x{B}: graph captured")
     ms = time_steps(graph.replay, steps, warmup, markers=markers)
@@ -789,6 +807,50 @@ def sorted_step_row(layers, aq, torch, steps, step_bytes, graph_ms, markers=Fals
             "host_sort_s": sort_s, "max_rel_l2_vs_row_major": err}
 
 
+def row_major_step_row(layers, graph, aq, torch, steps, step_bytes, graph_ms):
+    """The decode step over the row-major codes (aqlm_gemv_grouped /
+    aqlm_gemv), timed like the tiled graph `graph`; outputs compared bit for
+    bit with that graph's."""
+    graph.replay()
+    torch.cuda.synchronize()
+    ref = [L.y.clone() for L in layers]
+    g = graph_of(launches_by_dependency(layers, aq))
+    g.replay()
+    torch.cuda.synchronize()
+    same = all(torch.equal(a.view(torch.int16), L.y.view(torch.int16)) for a, L in zip(ref, layers))
+    del ref
+    ms = time_steps(g.replay, steps, 2)
+    del g
+    return {"ms_per_step": ms, "GBs": step_bytes / (ms * 1e6), "frac": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
+            "tiled_speedup": ms / graph_ms, "bit_identical_to_tiled": same}
+
+
+def tiled_step_row(layers, aq, torch, steps, step_bytes, graph_ms, markers=False):
+    """The decode step over tiled codes (aqlm_tile_codes once per layer, then
+    aqlm_gemv_grouped_tiled): grouped q/k/v, o, grouped gate/up, down, as one
+    graph; outputs compared bit for bit with the row-major graph's (which
+    the caller has just replayed)."""
+    import time
+    t0 = time.time()
+    tl = [aq.TiledCodes(L.codes, L.codebooks, L.scales) for L in layers]
+    torch.cuda.synchronize()
+    tile_s = time.time() - t0
+    ys = [torch.empty_like(L.y[0]) for L in layers]
+    launches = []
+    for b in range(0, len(layers), 7):
+        grp = lambda idx: (lambda: aq.gemv_tiled_grouped([(tl[i], layers[i].x[0], ys[i]) for i in idx]))
+        launches += [grp([b, b + 1, b + 2]), grp([b + 3]), grp([b + 4, b + 5]), grp([b + 6])]
+    g = graph_of(launches)
+    g.replay()
+    torch.cuda.synchronize()
+    same = all(torch.equal(y.view(torch.int16), L.y[0].view(torch.int16)) for y, L in zip(ys, layers))
+    ms = time_steps(g.replay, steps, 2, markers=markers)
+    del g, tl, ys
+    return {"ms_per_step": ms, "GBs": step_bytes / (ms * 1e6), "frac": step_bytes / (ms * 1e6) / HBM_PEAK_GBS,
+            "tok_s_eq": 1000.0 / ms, "launches": len(launches), "vs_row_major_graph": graph_ms / ms,
+            "bit_identical_to_row_major": same, "tile_s": tile_s}
+
+
 def step_seed(M: int) -> int:
     return 1000 * (1 if M == 2 else 2)
 
@@ -837,6 +899,16 @@ def main():
         row = persistent_step_row(layers, graph, aq, torch, args.steps, step_bytes, ms)
         print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "persistent_step": row}), flush=True)
         return
+    if args.tiled:
+        if B != 8:
+            sys.exit("bench.py: --tiled needs a workload with 8-bit codes")
+        layers, launches, graph, ms, spread, step_bytes = decode_step(model, M, B, step_seed(M), aq, args.steps,
+                                                                      args.warmup)
+        graph.replay()
+        torch.cuda.synchronize()
+        row = tiled_step_row(layers, aq, torch, args.steps, step_bytes, ms, markers=True)
+        print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "tiled_codes": row}), flush=True)
+        return
     if args.sorted:
         if B < 15:
             sys.exit("bench.py: --sorted needs a workload with 15- or 16-bit codes (llama2-7b-1x16)")
@@ -845,8 +917,10 @@ def main():
         row = sorted_step_row(layers, aq, torch, args.steps, step_bytes, ms, markers=True)
         print(json.dumps({"workload": args.workload, "graph_ms_per_step": ms, "sorted_codes": row}), flush=True)
         return
+    tiled = B == 8  # (8-bit codes: the step reads tiled codes)
     layers, launches, graph, ms, spread, step_bytes = decode_step(
-        model, M, B, step_seed(M), aq, args.steps, args.warmup, markers=True, spread_steps=args.spread_steps)
+        model, M, B, step_seed(M), aq, args.steps, args.warmup, markers=True, spread_steps=args.spread_steps,
+        tiled=tiled)
     log(f"{args.workload}: {len(layers)} layers in {len(launches)} launches, {step_bytes / 1e9:.3f} GB per step; "
         f"step {ms:.4f} ms (graph replay)")
 
@@ -891,7 +965,10 @@ def main():
         "config": {
             "workload": f"Llama-2-{model.upper()} decode step on one GPU, linear layers only, AQLM {M}x{B} "
                         f"g8, batch 1: {len(layers)} GEMVs in {len(launches)} launches (per block: grouped "
-                        f"q/k/v, o, grouped gate/up, down), replayed as one HIP graph",
+                        f"q/k/v, o, grouped gate/up, down), replayed as one HIP graph"
+                        + (", codes stored tiled (1 KiB tiles of 16 rows x 64 code bytes, written before "
+                           "timing)" if tiled else ""),
+            "code_layout": "tiled" if tiled else "row-major",
             "layers": len(layers),
             "launches": len(launches),
             "bytes_per_step": step_bytes,
@@ -915,15 +992,18 @@ def main():
             "source_digest": digest,
         },
     }
-    persistent = None
+    persistent = row_major = None
     if not args.no_secondary:
         persistent = persistent_step_row(layers, graph, aq, torch, max(5, args.steps // 2), step_bytes, ms)
         log(f"{args.workload} as one persistent launch: {persistent['ms_per_step']:.4f} ms per step")
+        if tiled:
+            row_major = row_major_step_row(layers, graph, aq, torch, max(5, args.steps // 2), step_bytes, ms)
+            log(f"{args.workload} over row-major codes: {row_major['ms_per_step']:.4f} ms per step")
     del layers, launches, graph
     torch.cuda.empty_cache()
 
     if not args.no_secondary:
-        sec = {"persistent_step": persistent}
+        sec = {"persistent_step": persistent, "row_major_codes": row_major}
         for other in ("llama2-7b-2x8", "llama2-7b-1x16"):
             if other == args.workload:
                 continue

@@ -164,6 +164,39 @@ enum aqlm_gemv_path {
 int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
                            int32_t path, void* stream);
 
+/* Tiled storage of 8-bit codes for the batch-1 product (the same codes b_ijm
+ * of Eq. 2 in another byte order; Sec. 4.3's token-generation product reads
+ * them).  Each wave of the product reads the 64-byte K-slice of 16 rows at a
+ * time; row-major, those are 16 separate half-lines, tiled they are one
+ * contiguous 1 KiB.  Layout, with row_bytes = (d_in / g) * M and
+ * ks = ceil(row_bytes / 64): byte c of row r at
+ *   ((r / 16) * ks + c / 64) * 1024 + (r % 16) * 64 + c % 64,
+ * rows past d_out and bytes past row_bytes zero.  Formats: B = 8, g = 8,
+ * M in {1, 2, 4}; anything else AQLM_ERR_UNSUPPORTED; shapes whose tiled
+ * size reaches 2^31 bytes AQLM_ERR_SHAPE. */
+
+/* Bytes of the tiled codes of one layer: 16 * ceil(d_out / 16) * ks * 64;
+ * 0 for an unsupported format or shape. */
+int64_t aqlm_tiled_codes_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g);
+
+/* Writes the tiled copy of row-major codes [d_out][d_in / g][M] (DEVICE,
+ * uint8, any alignment) to `tiled` (DEVICE, 16-byte aligned, caller-owned,
+ * at least aqlm_tiled_codes_bytes bytes: else AQLM_ERR_WORKSPACE) on
+ * `stream`.  NULL pointers AQLM_ERR_NULL.  Byte-exact permutation plus zero
+ * padding; allocates nothing. */
+int aqlm_tile_codes(const void* codes, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, void* tiled,
+                    int64_t tiled_bytes, void* stream);
+
+/* aqlm_gemv_grouped over tiled codes: each problem's `codes` points to what
+ * aqlm_tile_codes wrote for that layer (16-byte aligned), everything else as
+ * for aqlm_gemv_grouped (same validation order, errors, determinism).  The
+ * arithmetic is the gather kernel's on the same rows and workgroup split, so
+ * the results equal aqlm_gemv_grouped's on the row-major codes bit for bit.
+ * Formats beyond the tiled ones, or x too large for the kernel's on-chip
+ * staging (d_in above about 32768 for M = 2), return AQLM_ERR_UNSUPPORTED. */
+int aqlm_gemv_grouped_tiled(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                            void* stream);
+
 /* Product with n activation rows: y[t][i] = fp16(s_i * sum_c W[i][c] x[t][c])
  * with W reconstructed as above, fp32 accumulation, any n >= 1 (the batched
  * and prefill products of a layer; the paper times the single-row case,

@@ -187,6 +187,51 @@ def gemv_grouped(problems, *, path: str = "auto", stream=None):
     return [p[4] for p in problems]
 
 
+class TiledCodes:
+    """Tiled copy of a layer's 8-bit codes for the batch-1 product
+    (``aqlm_tile_codes`` / ``aqlm_gemv_grouped_tiled``): the codes of every
+    16 rows x 64-byte K-slice stored as one contiguous 1 KiB tile, written on
+    the GPU once.  ``codes``: uint8 [d_out, d_in/8, M] as for :func:`gemv`
+    (M of 1, 2 or 4, 2^8 codewords).  The products equal those over the
+    row-major codes bit for bit."""
+
+    def __init__(self, codes, codebooks, scales, *, stream=None):
+        d_out, d_in, M, B, g = _args(codes, codebooks, scales, None)
+        lib = _lib.load()
+        need = int(lib.aqlm_tiled_codes_bytes(d_out, d_in, M, B, g))
+        if need <= 0:
+            raise ValueError("tiled codes take 8-bit codes with M in {1, 2, 4} and g = 8")
+        self.codes = torch.empty(need, dtype=torch.uint8, device=codes.device)
+        _check(lib.aqlm_tile_codes(codes.data_ptr(), d_out, d_in, M, B, g, self.codes.data_ptr(), need,
+                                   _stream_handle(stream)), "aqlm_tile_codes")
+        self.codebooks, self.scales = codebooks, scales
+        self.d_out, self.d_in, self.M, self.B, self.g = d_out, d_in, M, B, g
+
+
+def gemv_tiled_grouped(problems, *, stream=None):
+    """Independent products [(tiled, x, y), ...] (``TiledCodes`` sharing
+    (M, B, g)) in one launch; each y [d_out] is written in place.  Returns
+    the y list."""
+    if not 1 <= len(problems) <= _lib.MAX_GROUPED:
+        raise ValueError(f"1..{_lib.MAX_GROUPED} problems per grouped launch")
+    arr = (_lib.GemvProblem * len(problems))()
+    fmt = None
+    for i, (t, x, y) in enumerate(problems):
+        if fmt is None:
+            fmt = (t.M, t.B, t.g)
+        elif fmt != (t.M, t.B, t.g):
+            raise ValueError("grouped problems must share (M, B, g)")
+        if x.dtype != torch.float16 or x.numel() != t.d_in or not x.is_cuda or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 GPU tensor with d_in elements")
+        if y.dtype != torch.float16 or y.numel() != t.d_out or not y.is_cuda or not y.is_contiguous():
+            raise ValueError("y must be a contiguous fp16 GPU tensor with d_out elements")
+        arr[i] = _lib.GemvProblem(t.codes.data_ptr(), t.codebooks.data_ptr(), t.scales.data_ptr(), x.data_ptr(),
+                                  y.data_ptr(), t.d_out, t.d_in)
+    st = _lib.load().aqlm_gemv_grouped_tiled(arr, len(problems), fmt[0], fmt[1], fmt[2], _stream_handle(stream))
+    _check(st, "aqlm_gemv_grouped_tiled")
+    return [p[2] for p in problems]
+
+
 def gemm_small_batch(codes, codebooks, scales, x, *, out=None, stream=None) -> torch.Tensor:
     """Y [n, d_out] = X W^T for fp16 activations X [n, d_in]."""
     d_out, d_in, M, B, g = layer_args(codes, codebooks, scales)

@@ -436,6 +436,59 @@ int aqlm_gemv_grouped_path(const aqlm_gemv_problem* problems, int32_t count, int
   return AQLM_OK;
 }
 
+// Tiled 8-bit codes: the format checks of check_layer, plus what the tiled
+// product reads (M of 1, 2 or 4; tiled offsets held in 31 bits).
+static int check_tiled_format(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t* bytes) {
+  if (d_out <= 0 || d_in <= 0 || g <= 0 || d_in % g != 0) return AQLM_ERR_SHAPE;
+  if (g != 8 || B != 8 || !aqlm::gemv_mfma_supported(M, B)) return AQLM_ERR_UNSUPPORTED;
+  if (d_out >= (int64_t(1) << 31) || d_in >= (int64_t(1) << 31)) return AQLM_ERR_SHAPE;
+  *bytes = aqlm::tiled_codes_bytes(d_out, d_in / g * M);
+  if (*bytes >= (int64_t(1) << 31)) return AQLM_ERR_SHAPE;
+  return AQLM_OK;
+}
+
+int64_t aqlm_tiled_codes_bytes(int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g) {
+  int64_t bytes = 0;
+  return check_tiled_format(d_out, d_in, M, B, g, &bytes) == AQLM_OK ? bytes : 0;
+}
+
+int aqlm_tile_codes(const void* codes, int64_t d_out, int64_t d_in, int32_t M, int32_t B, int32_t g, void* tiled,
+                    int64_t tiled_bytes, void* stream) {
+  if (!codes || !tiled) return AQLM_ERR_NULL;
+  int64_t need = 0;
+  const int st = check_tiled_format(d_out, d_in, M, B, g, &need);
+  if (st != AQLM_OK) return st;
+  if (tiled_bytes < need) return AQLM_ERR_WORKSPACE;
+  if (!aligned(tiled, 16)) return AQLM_ERR_ALIGN;
+  return status_of(aqlm::launch_tile_codes(static_cast<const uint8_t*>(codes), d_out, d_in / g * M,
+                                           static_cast<uint8_t*>(tiled), static_cast<hipStream_t>(stream)));
+}
+
+int aqlm_gemv_grouped_tiled(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
+                            void* stream) {
+  if (!problems) return AQLM_ERR_NULL;
+  if (count < 1 || count > AQLM_MAX_GROUPED) return AQLM_ERR_SHAPE;
+  aqlm::Layer Ls[AQLM_MAX_GROUPED];
+  const uint16_t* xs[AQLM_MAX_GROUPED];
+  uint16_t* ys[AQLM_MAX_GROUPED];
+  for (int i = 0; i < count; ++i) {
+    const aqlm_gemv_problem& P = problems[i];
+    int64_t bytes = 0;
+    int st = check_tiled_format(P.d_out, P.d_in, M, B, g, &bytes);
+    if (st != AQLM_OK) return st;
+    st = check_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &Ls[i]);
+    if (st != AQLM_OK) return st;
+    if (!P.x || !P.y) return AQLM_ERR_NULL;
+    if (!aligned(P.x, 16) || !aligned(P.y, 16)) return AQLM_ERR_ALIGN;
+    Ls[i].tiled = true;
+    Ls[i].vec_codes = true;  // (tiles are whole 64-byte K-slices at 16-byte aligned addresses)
+    xs[i] = P.x;
+    ys[i] = P.y;
+  }
+  if (!aqlm::gemv_mfma_fits(Ls, count)) return AQLM_ERR_UNSUPPORTED;
+  return status_of(aqlm::launch_gemv_mfma(Ls, xs, ys, count, static_cast<hipStream_t>(stream)));
+}
+
 int64_t aqlm_gemv_step_plan_bytes(int32_t levels) {
   if (levels < 1 || levels > AQLM_STEP_MAX_LEVELS) return 0;
   return (int64_t)sizeof(aqlm::StepHeader) + (int64_t)levels * (int64_t)sizeof(aqlm::StepLevel);

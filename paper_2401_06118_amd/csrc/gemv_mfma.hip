@@ -373,7 +373,12 @@ __device__ __forceinline__ bool ks_body(const GemvBatch& bt, const int vwg, Wait
   const int KS = (int)((pitch + 63u) / 64u);        // 64-byte K-slices per row
   const int xg = KS * (C::kKS / M);
   const int nks = KS > wave ? (KS - wave + kWaves - 1) / kWaves : 0;
-  const uint8_t* __restrict__ wg_codes = bt.p[p].codes + (size_t)row0 * pitch;
+  // Row-major codes: a wave's item is 16 rows x 64 bytes at the row pitch.
+  // Tiled codes: the same item is one contiguous 1 KiB tile.
+  const bool tiled = bt.tiled != 0;
+  const uint8_t* __restrict__ wg_codes = tiled ? bt.p[p].codes : bt.p[p].codes + (size_t)row0 * pitch;
+  const uint32_t k_stride = tiled ? 1024u : 64u;   // bytes from one K-slice to the next
+  const uint32_t k_limit = tiled ? 0xFFFFFFFFu : pitch;  // (tiles hold whole K-slices)
 
   uint4* cb_lds = lds;
   uint4* x_lds = lds + M * 256 * COPIES;
@@ -416,15 +421,18 @@ __device__ __forceinline__ bool ks_body(const GemvBatch& bt, const int vwg, Wait
   int row_off[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const int row = rb * 16 + r16;
-    row_off[rb] = (row < rows ? row : rows - 1) * (int)pitch;
+    int row = rb * 16 + r16;
+    row = row < rows ? row : rows - 1;
+    const int grow = row0 + row;
+    row_off[rb] = tiled ? (grow >> 4) * KS * 1024 + (grow & 15) * 64 : row * (int)pitch;
   }
   auto issue_rb = [&](int j, int rb, uint32_t (&w)[4]) {
     const bool past = j >= nks;  // (wave-uniform)
     const int jj = past ? (nks > 0 ? nks - 1 : 0) : j;
-    const uint32_t off = (uint32_t)(wave + jj * kWaves) * 64u + slot_off;
+    const uint32_t ks_off = (uint32_t)(wave + jj * kWaves) * 64u + slot_off;  // in a row-major row
+    const uint32_t off = (uint32_t)(wave + jj * kWaves) * k_stride + slot_off;
     if constexpr (VEC) {
-      const uint32_t o = (uint32_t)row_off[rb] + (off < pitch ? off : 0u);
+      const uint32_t o = (uint32_t)row_off[rb] + (ks_off < k_limit ? off : 0u);
       // A load past the wave's last K-slice only keeps the count of loads in
       // flight exact; its value is never used.  It reads the codebook, which
       // every workgroup has just read and L2 holds, not the last K-slice
@@ -1127,7 +1135,9 @@ hipError_t gemv_mfma_impl(const Layer* Ls, const uint16_t* const* xs, uint16_t* 
   const int M = Ls[0].M, B = Ls[0].B;
   const bool packed = Ls[0].packed;
   for (int i = 1; i < count; ++i)
-    if (Ls[i].packed != packed) return hipErrorInvalidValue;
+    if (Ls[i].packed != packed || Ls[i].tiled != Ls[0].tiled) return hipErrorInvalidValue;
+  // tiled codes: 8-bit, 16-byte aligned, read by k_gemv_ks alone
+  if (Ls[0].tiled && (B != 8 || packed || plan || !Ls[0].vec_codes)) return hipErrorInvalidValue;
   const int kCPL = (B == 8) ? 16 : 8, kKS = 4 * kCPL;
   bool vec = true;
   double total_bytes = 0;
@@ -1188,6 +1198,7 @@ hipError_t gemv_mfma_impl(const Layer* Ls, const uint16_t* const* xs, uint16_t* 
   }
   GemvBatch bt{};
   bt.count = count;
+  bt.tiled = Ls[0].tiled ? 1 : 0;
   int wg = 0, ni_max = 1, xg_max = 0, rb_max = 1, nks_min = 1 << 30;
   for (int i = 0; i < count; ++i) {
     const Layer& L = Ls[i];

@@ -32,7 +32,19 @@ struct Layer {
   int32_t B;
   bool vec_codes;  // codes base 16-byte aligned and row pitch a multiple of 16 bytes
   bool packed;     // B-bit codes packed into a bit string per row (32-bit words; B = 12, 15)
+  bool tiled = false;  // 8-bit codes in 1 KiB tiles (tiled_codes_offset), not row-major
 };
+
+// Tiled 8-bit codes: the code bytes of 16 rows x one 64-byte K-slice of a row
+// are one 1 KiB tile, row after row; tiles run K-slice after K-slice within a
+// 16-row block, then block after block.  Rows past d_out and bytes past a
+// row's G * M are zero.  Byte c of row r sits at this offset.
+inline int64_t tiled_codes_offset(int64_t r, int64_t c, int64_t ks_per_row) {
+  return ((r >> 4) * ks_per_row + (c >> 6)) * 1024 + (r & 15) * 64 + (c & 63);
+}
+inline int64_t tiled_codes_bytes(int64_t d_out, int64_t row_bytes) {
+  return ((d_out + 15) / 16) * ((row_bytes + 63) / 64) * 1024;
+}
 
 // 32-bit words of one row of packed codes: G*M codes of B bits, zero-padded.
 inline int32_t packed_row_words(int32_t G, int32_t M, int32_t B) {
@@ -61,6 +73,7 @@ struct GemvBatch {
   int32_t count;
   int32_t total_wgs;
   int32_t xg_max;  // x groups staged in LDS by the largest problem
+  int32_t tiled;   // codes of every problem tiled (k_gemv_ks only)
 };
 
 // Decode step (a persistent launch over many grouped 2x8 products): one
@@ -92,6 +105,9 @@ hipError_t launch_step(const StepLevel* levels, int32_t nlev, int32_t grid, size
 hipError_t launch_dequant(const Layer& L, uint16_t* w, hipStream_t s);
 bool gemv_mfma_supported(int M, int B);
 bool gemv_mfma_fits(const Layer* Ls, int count);
+// Row-major 8-bit codes [d_out][row_bytes] to the tiled layout (csrc/tiled.hip).
+hipError_t launch_tile_codes(const uint8_t* codes, int64_t d_out, int64_t row_bytes, uint8_t* tiled, hipStream_t s);
+
 hipError_t launch_gemv_mfma(const Layer* Ls, const uint16_t* const* xs, uint16_t* const* ys, int count,
                             hipStream_t s);
 hipError_t launch_gemv(const Layer& L, const uint16_t* x, uint16_t* y, hipStream_t s);

@@ -347,3 +347,44 @@ def test_large_groups_accepted_only_where_supported(lib):
     buf = ctypes.create_string_buffer(nbytes)
     one = (ctypes.c_int32 * 1)(1)
     assert lib.aqlm_gemv_step_plan(arr, one, 1, 4, 8, 16, ctypes.addressof(buf), nbytes) == UNSUP
+
+
+def tiled_bytes_by_definition(d_out, d_in, M):
+    """Tiles of 16 rows x 64 code bytes, 1 KiB each, rows and row bytes
+    rounded up to whole tiles."""
+    row_bytes = d_in // 8 * M
+    return -(-d_out // 16) * -(-row_bytes // 64) * 1024
+
+
+def test_tiled_codes_validation(lib):
+    """Tiled 8-bit codes: the size query, and bad arguments refused before
+    anything is launched (fake pointers)."""
+    for d_out, d_in, M in ((64, 256, 2), (37, 200, 2), (8192, 28672, 2), (1, 8, 1), (100, 520, 4)):
+        assert lib.aqlm_tiled_codes_bytes(d_out, d_in, M, 8, 8) == tiled_bytes_by_definition(d_out, d_in, M)
+    assert lib.aqlm_tiled_codes_bytes(64, 256, 3, 8, 8) == 0        # M = 3: no matrix-core kernel
+    assert lib.aqlm_tiled_codes_bytes(64, 256, 1, 16, 8) == 0       # 16-bit codes
+    assert lib.aqlm_tiled_codes_bytes(64, 256, 2, 8, 16) == 0       # groups of 16
+    assert lib.aqlm_tiled_codes_bytes(0, 256, 2, 8, 8) == 0
+    assert lib.aqlm_tiled_codes_bytes(64, 252, 2, 8, 8) == 0
+    assert lib.aqlm_tiled_codes_bytes(1 << 20, 1 << 15, 4, 8, 8) == 0  # 2^31 bytes or more
+    need = tiled_bytes_by_definition(64, 256, 2)
+    assert lib.aqlm_tile_codes(None, 64, 256, 2, 8, 8, P, need, None) == NULL
+    assert lib.aqlm_tile_codes(P, 64, 256, 2, 8, 8, None, need, None) == NULL
+    assert lib.aqlm_tile_codes(P, 64, 256, 2, 8, 8, P, need - 1, None) == WORKSPACE
+    assert lib.aqlm_tile_codes(P, 64, 256, 2, 8, 8, P + 8, need, None) == ALIGN
+    assert lib.aqlm_tile_codes(P, 64, 256, 2, 16, 8, P, need, None) == UNSUP
+    assert lib.aqlm_tile_codes(P, 64, 250, 2, 8, 8, P, need, None) == SHAPE
+    Prob = _lib.GemvProblem
+    good = Prob(P, P, P, P, P, 64, 256)
+    arr = (Prob * 9)(*([good] * 9))
+    assert lib.aqlm_gemv_grouped_tiled(None, 1, 2, 8, 8, None) == NULL
+    assert lib.aqlm_gemv_grouped_tiled(arr, 0, 2, 8, 8, None) == SHAPE
+    assert lib.aqlm_gemv_grouped_tiled(arr, 9, 2, 8, 8, None) == SHAPE
+    assert lib.aqlm_gemv_grouped_tiled(arr, 2, 3, 8, 8, None) == UNSUP
+    assert lib.aqlm_gemv_grouped_tiled(arr, 2, 1, 16, 8, None) == UNSUP
+    bad = (Prob * 2)(good, Prob(P, P, P, P, P, 64, 60))
+    assert lib.aqlm_gemv_grouped_tiled(bad, 2, 2, 8, 8, None) == SHAPE
+    bad = (Prob * 2)(good, Prob(P + 8, P, P, P, P, 64, 256))
+    assert lib.aqlm_gemv_grouped_tiled(bad, 2, 2, 8, 8, None) == ALIGN
+    bad = (Prob * 2)(good, Prob(P, P, P, P, None, 64, 256))
+    assert lib.aqlm_gemv_grouped_tiled(bad, 2, 2, 8, 8, None) == NULL
