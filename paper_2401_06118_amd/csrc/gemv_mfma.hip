@@ -349,8 +349,13 @@ __device__ __forceinline__ bool ks_body(const GemvBatch& bt, const int vwg, Wait
   // keep about 8 MiB in flight across the chip.  Measured (same box):
   // Llama-2-70B step 5.38-5.41 ms with two ahead, 5.50-5.51 with three,
   // 5.87-5.90 with four (five or six slower still); 7B step 0.853 / 0.906 /
-  // 0.888 ms.  Single blocks: the whole ring (four ahead measured the same).
-  constexpr int kAheadWant = RB >= 2 ? 2 : 8;
+  // 0.888 ms.  An odd block count ends each K-slice with a lone block, which
+  // requests one item, so the next pair's first item would be asked for only
+  // one item before its use: three ahead there (tiled codes: Llama-2-70B
+  // q/k/v, 3 blocks, 9.2 -> 8.5 us, gate/up, 7 blocks, 29.7 -> 28.8 us; step
+  // 5.30-5.32 -> 5.21-5.22 ms, 7B unchanged).  Single blocks: the whole ring
+  // (four ahead measured the same).
+  constexpr int kAheadWant = RB >= 2 ? (RB % 2 == 1 ? 3 : 2) : 8;
   constexpr int kAhead = kAheadWant < kSlots ? kAheadWant : kSlots;
   static_assert(RB < 2 || kAhead >= 2, "both items of a pair must be requested before the pair starts");
   extern __shared__ uint4 lds[];
