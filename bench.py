@@ -1016,6 +1016,9 @@ def main():
                    "GBs_event_pair": ob / (sum(pair) * 1e6)}
             if oM == 2:
                 row["persistent_step"] = persistent_step_row(ol, og, aq, torch, max(5, args.steps // 2), ob, oms)
+                og.replay()
+                torch.cuda.synchronize()
+                row["tiled_codes"] = tiled_step_row(ol, aq, torch, max(5, args.steps // 2), ob, oms)
                 # the same step without grouping (224 single launches), and
                 # without the block's dependencies (8 independent GEMVs per launch)
                 g1 = graph_of([lambda L=L: L.gemv(aq) for L in ol])
