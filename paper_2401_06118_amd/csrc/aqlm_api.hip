@@ -473,10 +473,10 @@ int aqlm_gemv_grouped_tiled(const aqlm_gemv_problem* problems, int32_t count, in
   uint16_t* ys[AQLM_MAX_GROUPED];
   for (int i = 0; i < count; ++i) {
     const aqlm_gemv_problem& P = problems[i];
-    int64_t bytes = 0;
-    int st = check_tiled_format(P.d_out, P.d_in, M, B, g, &bytes);
+    int st = check_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &Ls[i]);
     if (st != AQLM_OK) return st;
-    st = check_layer(P.codes, P.codebooks, P.scales, P.d_out, P.d_in, M, B, g, &Ls[i]);
+    int64_t bytes = 0;  // (the formats and sizes tiled codes take)
+    st = check_tiled_format(P.d_out, P.d_in, M, B, g, &bytes);
     if (st != AQLM_OK) return st;
     if (!P.x || !P.y) return AQLM_ERR_NULL;
     if (!aligned(P.x, 16) || !aligned(P.y, 16)) return AQLM_ERR_ALIGN;

@@ -388,3 +388,14 @@ def test_tiled_codes_validation(lib):
     assert lib.aqlm_gemv_grouped_tiled(bad, 2, 2, 8, 8, None) == ALIGN
     bad = (Prob * 2)(good, Prob(P, P, P, P, None, 64, 256))
     assert lib.aqlm_gemv_grouped_tiled(bad, 2, 2, 8, 8, None) == NULL
+
+
+def test_tiled_grouped_validation_order(lib):
+    """aqlm_gemv_grouped_tiled reports what aqlm_gemv_grouped reports first
+    (a NULL pointer before an unsupported format)."""
+    Prob = _lib.GemvProblem
+    arr = (Prob * 1)(Prob(None, P, P, P, P, 64, 256))
+    assert lib.aqlm_gemv_grouped(arr, 1, 1, 16, 8, None) == NULL
+    assert lib.aqlm_gemv_grouped_tiled(arr, 1, 1, 16, 8, None) == NULL
+    arr = (Prob * 1)(Prob(P, P, P, P, P, 64, 60))
+    assert lib.aqlm_gemv_grouped_tiled(arr, 1, 3, 8, 8, None) == SHAPE
