@@ -609,10 +609,11 @@ PATH_CASES = {
 
 
 def compare_paths(aq, torch, once=False):
-    """Both kernel families on the same launches: each case's grouped launch
-    rotated over >= 1 GiB of independent layers (so HBM is read), timed per
-    launch from a graph of the rotation; plus the relative L2 difference of
-    the two results."""
+    """Both kernel families on the same launches, and the gather kernel over
+    tiled codes: each case's grouped launch rotated over >= 1 GiB of
+    independent layers (so HBM is read), timed per launch from a graph of the
+    rotation; plus the relative L2 difference of the two families' results
+    and whether the tiled product equals the row-major one bit for bit."""
     from paper_2401_06118_amd import format as fmt
     rows = []
     for name, shapes in PATH_CASES.items():
@@ -640,6 +641,21 @@ def compare_paths(aq, torch, once=False):
                 res[f"{path}_GBs"] = b / (us * 1e3)
             outs[path] = [L.y.double().clone() for L in sets[0]]
         res["rel_l2_diff"] = max(float((a - c).norm() / c.norm()) for a, c in zip(outs["table"], outs["gather"]))
+        # the gather kernel over tiled codes (same arithmetic: bit-identical)
+        tsets = [[aq.TiledCodes(L.codes, L.codebooks, L.scales) for L in ls] for ls in sets]
+        calls = [lambda ls=ls, ts=ts: aq.gemv_tiled_grouped([(t, L.x[0], L.y[0]) for t, L in zip(ts, ls)])
+                 for ls, ts in zip(sets, tsets)]
+        if once:
+            calls[0]()
+            torch.cuda.synchronize()
+        else:
+            g = graph_of(calls)
+            us = time_steps(g.replay, steps=5, warmup=1) / reps * 1e3
+            del g
+            res["tiled_us"] = us
+            res["tiled_GBs"] = b / (us * 1e3)
+        res["tiled_bit_identical"] = all(torch.equal(L.y.double(), r) for L, r in zip(sets[0], outs["gather"]))
+        del tsets
         rows.append(res)
         log(f"{name}: " + ", ".join(f"{k} {v:.2f}" for k, v in res.items() if k.endswith("_us")))
         del sets
