@@ -509,6 +509,17 @@ def batch_rows(aq, torch, cases=None):
                 rows.append({"layer": name, "n": n, "us": ms * 1e3,
                              "GBs": b / (ms * 1e6), "TFLOPs": shp.flops(n) / (ms * 1e9),
                              "mfma_frac": shp.flops(n) / (ms * 1e9) / MFMA_F16_PEAK_TFS})
+                if B == 8 and n <= 16:
+                    # the same products over tiled codes (aqlm_gemm_small_batch_tiled)
+                    ref = [L.y.clone() for L in layers]
+                    tl = [aq.TiledCodes(L.codes, L.codebooks, L.scales) for L in layers]
+                    g = graph_of([lambda L=L, t=t: t.gemm_small_batch(L.x, out=L.y) for L, t in zip(layers, tl)])
+                    ms = time_steps(g.replay, steps=max(3, 8 // reps), warmup=1) / reps
+                    del g
+                    same = all(torch.equal(r.view(torch.int16), L.y.view(torch.int16)) for r, L in zip(ref, layers))
+                    rows.append({"layer": name, "n": n, "op": "tiled codes", "us": ms * 1e3,
+                                 "GBs": b / (ms * 1e6), "bit_identical_to_row_major": same})
+                    del ref, tl
                 del layers
                 torch.cuda.empty_cache()
             # the workspace path (aqlm_gemm: dequantize once, dense fp16 product)

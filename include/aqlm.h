@@ -197,6 +197,16 @@ int aqlm_tile_codes(const void* codes, int64_t d_out, int64_t d_in, int32_t M, i
 int aqlm_gemv_grouped_tiled(const aqlm_gemv_problem* problems, int32_t count, int32_t M, int32_t B, int32_t g,
                             void* stream);
 
+/* aqlm_gemm_small_batch over tiled codes (what aqlm_tile_codes wrote for the
+ * layer, 16-byte aligned) for 1 to 16 activation rows, the token-generation
+ * product of Sec. 4.3 with several sequences: n = 1 as aqlm_gemv, 2 <= n <= 16
+ * with M in {2, 4} by the small-batch kernel.  Validation, errors and results
+ * as aqlm_gemm_small_batch on the row-major codes (bit for bit); other n or
+ * M (M = 1 with n > 1) AQLM_ERR_UNSUPPORTED before anything is launched. */
+int aqlm_gemm_small_batch_tiled(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                                int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x,
+                                uint16_t* y, void* stream);
+
 /* Product with n activation rows: y[t][i] = fp16(s_i * sum_c W[i][c] x[t][c])
  * with W reconstructed as above, fp32 accumulation, any n >= 1 (the batched
  * and prefill products of a layer; the paper times the single-row case,

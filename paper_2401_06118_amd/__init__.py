@@ -207,6 +207,21 @@ class TiledCodes:
         self.codebooks, self.scales = codebooks, scales
         self.d_out, self.d_in, self.M, self.B, self.g = d_out, d_in, M, B, g
 
+    def gemm_small_batch(self, x, *, out=None, stream=None) -> torch.Tensor:
+        """Y [n, d_out] = X W^T for fp16 activations X [n, d_in], 1 <= n <= 16
+        (n > 1 needs M of 2 or 4): what :func:`gemm_small_batch` computes on
+        the row-major codes, bit for bit."""
+        if x.dtype != torch.float16 or x.dim() != 2 or x.shape[1] != self.d_in or not x.is_cuda \
+                or not x.is_contiguous():
+            raise ValueError("x must be a contiguous fp16 GPU tensor [n, d_in]")
+        n = x.shape[0]
+        out = _out(out, (n, self.d_out), self.codes)
+        st = _lib.load().aqlm_gemm_small_batch_tiled(self.codes.data_ptr(), self.codebooks.data_ptr(),
+                                                     self.scales.data_ptr(), self.d_out, self.d_in, self.M, self.B,
+                                                     self.g, n, x.data_ptr(), out.data_ptr(), _stream_handle(stream))
+        _check(st, "aqlm_gemm_small_batch_tiled")
+        return out
+
 
 def gemv_tiled_grouped(problems, *, stream=None):
     """Independent products [(tiled, x, y), ...] (``TiledCodes`` sharing

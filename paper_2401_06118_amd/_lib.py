@@ -24,7 +24,7 @@ EXPORTS = ("aqlm_dequantize", "aqlm_gemv", "aqlm_gemv_grouped", "aqlm_gemv_group
            "aqlm_packed_row_words", "aqlm_gemv_step_plan_bytes", "aqlm_gemv_step_plan", "aqlm_gemv_step",
            "aqlm_gemv_step_status", "aqlm_sort_codes_size", "aqlm_sort_codes", "aqlm_gemv_sorted_workspace_bytes",
            "aqlm_gemv_sorted", "aqlm_gemv_sorted_grouped", "aqlm_status_string", "aqlm_tiled_codes_bytes",
-           "aqlm_tile_codes", "aqlm_gemv_grouped_tiled")
+           "aqlm_tile_codes", "aqlm_gemv_grouped_tiled", "aqlm_gemm_small_batch_tiled")
 MAX_GROUPED = 8
 PACKED = 0x100  # OR-ed into B: bit-packed codes
 STEP_SYNC_BYTES = 256
@@ -81,6 +81,8 @@ def load():
         lib.aqlm_tile_codes.restype = ctypes.c_int
         lib.aqlm_gemv_grouped_tiled.argtypes = [ctypes.POINTER(GemvProblem), i32, i32, i32, i32, p]
         lib.aqlm_gemv_grouped_tiled.restype = ctypes.c_int
+        lib.aqlm_gemm_small_batch_tiled.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p]
+        lib.aqlm_gemm_small_batch_tiled.restype = ctypes.c_int
         lib.aqlm_gemm_small_batch.argtypes = [p, p, p, i64, i64, i32, i32, i32, i64, p, p, p]
         lib.aqlm_gemm_small_batch.restype = ctypes.c_int
         lib.aqlm_gemm_workspace_bytes.argtypes = [i64, i64, i32, i32, i32, i64]

@@ -489,6 +489,28 @@ int aqlm_gemv_grouped_tiled(const aqlm_gemv_problem* problems, int32_t count, in
   return status_of(aqlm::launch_gemv_mfma(Ls, xs, ys, count, static_cast<hipStream_t>(stream)));
 }
 
+int aqlm_gemm_small_batch_tiled(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
+                                int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x,
+                                uint16_t* y, void* stream) {
+  aqlm::Layer L;
+  int st = check_layer(codes, codebooks, scales, d_out, d_in, M, B, g, &L);
+  if (st != AQLM_OK) return st;
+  st = check_tokens(x, y, n, d_in);
+  if (st != AQLM_OK) return st;
+  int64_t bytes = 0;
+  st = check_tiled_format(d_out, d_in, M, B, g, &bytes);
+  if (st != AQLM_OK) return st;
+  L.tiled = true;
+  L.vec_codes = true;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n == 1) {
+    if (!aqlm::gemv_mfma_fits(&L, 1)) return AQLM_ERR_UNSUPPORTED;
+    return status_of(aqlm::launch_gemv_mfma(&L, &x, &y, 1, s));
+  }
+  if (!aqlm::gemm_nb_supported(L, (int32_t)n)) return AQLM_ERR_UNSUPPORTED;
+  return status_of(aqlm::launch_gemm_nb(L, (int32_t)n, x, y, s));
+}
+
 int64_t aqlm_gemv_step_plan_bytes(int32_t levels) {
   if (levels < 1 || levels > AQLM_STEP_MAX_LEVELS) return 0;
   return (int64_t)sizeof(aqlm::StepHeader) + (int64_t)levels * (int64_t)sizeof(aqlm::StepLevel);

@@ -46,6 +46,7 @@ struct GemmNbArgs {
   int32_t G;
   int32_t n;
   int32_t rows_per_wg;
+  int32_t tiled;  // codes in 1 KiB tiles (tiled_codes_offset), not row-major
 };
 
 template <int M>
@@ -87,7 +88,12 @@ __global__ __launch_bounds__(kThreadsNB) void k_gemm_nb(const GemmNbArgs a) {
   const int KS = (int)((pitch + 63u) / 64u);     // 64-byte K-slices per row
   const int R = (KS + kWavesNB - 1) / kWavesNB;  // rounds (the same for every wave)
   const int nks = KS > wave ? (KS - wave + kWavesNB - 1) / kWavesNB : 0;  // rounds with a K-slice for this wave
-  const uint8_t* __restrict__ wg_codes = a.codes + (size_t)row0 * pitch;
+  // Row-major codes: an item is 16 rows x 64 bytes at the row pitch; tiled
+  // codes: the same item is one contiguous 1 KiB tile.
+  const bool tiled = a.tiled != 0;
+  const uint8_t* __restrict__ wg_codes = tiled ? a.codes : a.codes + (size_t)row0 * pitch;
+  const uint32_t k_stride = tiled ? 1024u : 64u;         // bytes from one K-slice to the next
+  const uint32_t k_limit = tiled ? 0xFFFFFFFFu : pitch;  // (tiles hold whole K-slices)
 
   uint4* cb_lds = lds;
   uint4* x_lds = lds + M * 256 * COPIES;                        // [n][kXG]
@@ -122,13 +128,16 @@ __global__ __launch_bounds__(kThreadsNB) void k_gemm_nb(const GemmNbArgs a) {
   int row_off[RB];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const int row = rb * 16 + r16;
-    row_off[rb] = (row < rows ? row : rows - 1) * (int)pitch;
+    int row = rb * 16 + r16;
+    row = row < rows ? row : rows - 1;
+    const int grow = row0 + row;
+    row_off[rb] = tiled ? (grow >> 4) * KS * 1024 + (grow & 15) * 64 : row * (int)pitch;
   }
   auto issue_rb = [&](int j, int rb, uint32_t (&w)[4]) {
-    const uint32_t off = (uint32_t)(wave + j * kWavesNB) * 64u + slot_off;
+    const uint32_t ks_off = (uint32_t)(wave + j * kWavesNB) * 64u + slot_off;  // in a row-major row
+    const uint32_t off = (uint32_t)(wave + j * kWavesNB) * k_stride + slot_off;
     if constexpr (VEC) {
-      const uint32_t o = (uint32_t)row_off[rb] + (off < pitch ? off : 0u);
+      const uint32_t o = (uint32_t)row_off[rb] + (ks_off < k_limit ? off : 0u);
       const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(wg_codes + o));
       w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
     } else {
@@ -314,7 +323,7 @@ bool gemm_nb_supported(const Layer& L, int32_t n) {
 }
 
 hipError_t launch_gemm_nb(const Layer& L, int32_t n, const uint16_t* x, uint16_t* y, hipStream_t s) {
-  if (!gemm_nb_supported(L, n)) return hipErrorInvalidValue;
+  if (!gemm_nb_supported(L, n) || (L.tiled && !L.vec_codes)) return hipErrorInvalidValue;
   const int M = L.M;
   const int cus = num_cus();
   // One workgroup per CU when the rows allow it; at most nb_rb_cap(M) row
@@ -333,7 +342,7 @@ hipError_t launch_gemm_nb(const Layer& L, int32_t n, const uint16_t* x, uint16_t
   while (copies > 1 && fixed + per_copy * copies > kLdsLimit) copies /= 2;
   const size_t lds = fixed + per_copy * copies;
   GemmNbArgs a{static_cast<const uint8_t*>(L.codes), reinterpret_cast<const uint4*>(L.codebooks), L.scales,
-               reinterpret_cast<const uint4*>(x), y, L.d_out, L.G, n, rows_per_wg};
+               reinterpret_cast<const uint4*>(x), y, L.d_out, L.G, n, rows_per_wg, L.tiled ? 1 : 0};
   const bool vec = L.vec_codes;
   switch (M) {
     case 2: return vec ? launch_nb_copies<2, true>(a, nwg, rb, rounds, copies, lds, s)

@@ -171,3 +171,42 @@ def test_tiled_errors():
     assert torch.all(y == 5.0)
     with pytest.raises(ValueError):
         aq().TiledCodes(*to_device(synth.layer(9801, 64, 256, 1, 16))[:3])
+
+
+# Small batch over tiled codes: (d_out, d_in, M, n) - ragged rows and
+# K-slices, the unaligned-pitch class, 7B shapes, 1..16 rows.
+NB_CASES = [(37, 200, 2, 2), (1000, 4104, 2, 3), (100, 1032, 4, 16), (4096, 4096, 2, 4), (11008, 4096, 4, 16),
+            (4096, 11008, 2, 8), (256, 1024, 2, 1), (256, 1024, 1, 1)]
+
+
+@pytest.mark.parametrize("d_out,d_in,M,n", NB_CASES)
+def test_gemm_small_batch_tiled(d_out, d_in, M, n):
+    print(f"[tiled small batch] {d_out}x{d_in} M={M} n={n}", flush=True)
+    lay = synth.layer(9900 + d_out + M + n, d_out, d_in, M, 8, n=n)
+    codes, cb, sc, x = to_device(lay)
+    y_rm = aq().gemm_small_batch(codes, cb, sc, x)
+    t = aq().TiledCodes(codes, cb, sc)
+    y_t = t.gemm_small_batch(x)
+    torch.cuda.synchronize()
+    got = fp16_to_np(y_t)
+    rows = None
+    if d_out > 4096:
+        rows = np.unique(np.concatenate([[0, d_out - 1], np.random.default_rng(11).integers(0, d_out, 64)]))
+    check_products(lay, got, rows)
+    assert np.array_equal(got.view(np.uint16), fp16_to_np(y_rm).view(np.uint16))
+
+
+def test_gemm_small_batch_tiled_refusals():
+    lay = synth.layer(9990, 64, 256, 1, 8, n=2)
+    codes, cb, sc, x = to_device(lay)
+    t = aq().TiledCodes(codes, cb, sc)
+    with pytest.raises(RuntimeError):
+        t.gemm_small_batch(x)  # M = 1 with two rows
+    lay = synth.layer(9991, 64, 256, 2, 8, n=17)
+    codes, cb, sc, x = to_device(lay)
+    t = aq().TiledCodes(codes, cb, sc)
+    out = torch.full((17, 64), 5.0, dtype=torch.float16, device="cuda")
+    with pytest.raises(RuntimeError):
+        t.gemm_small_batch(x, out=out)  # more than 16 rows
+    torch.cuda.synchronize()
+    assert torch.all(out == 5.0)
