@@ -198,11 +198,12 @@ int aqlm_gemv_grouped_tiled(const aqlm_gemv_problem* problems, int32_t count, in
                             void* stream);
 
 /* aqlm_gemm_small_batch over tiled codes (what aqlm_tile_codes wrote for the
- * layer, 16-byte aligned) for 1 to 16 activation rows, the token-generation
- * product of Sec. 4.3 with several sequences: n = 1 as aqlm_gemv, 2 <= n <= 16
- * with M in {2, 4} by the small-batch kernel.  Validation, errors and results
- * as aqlm_gemm_small_batch on the row-major codes (bit for bit); other n or
- * M (M = 1 with n > 1) AQLM_ERR_UNSUPPORTED before anything is launched. */
+ * layer, 16-byte aligned) for 1 to 64 activation rows, the token-generation
+ * product of Sec. 4.3 with several sequences: n = 1 as aqlm_gemv; 2 <= n <= 64
+ * with M in {2, 4} by the small-batch kernel, up to 16 rows per launch (a
+ * last chunk of one row as aqlm_gemv).  Validation, errors and results as
+ * aqlm_gemm_small_batch on the row-major codes (bit for bit); n > 64, or
+ * M = 1 with n > 1, AQLM_ERR_UNSUPPORTED before anything is launched. */
 int aqlm_gemm_small_batch_tiled(const void* codes, const uint16_t* codebooks, const uint16_t* scales, int64_t d_out,
                                 int64_t d_in, int32_t M, int32_t B, int32_t g, int64_t n, const uint16_t* x,
                                 uint16_t* y, void* stream);

@@ -208,7 +208,7 @@ class TiledCodes:
         self.d_out, self.d_in, self.M, self.B, self.g = d_out, d_in, M, B, g
 
     def gemm_small_batch(self, x, *, out=None, stream=None) -> torch.Tensor:
-        """Y [n, d_out] = X W^T for fp16 activations X [n, d_in], 1 <= n <= 16
+        """Y [n, d_out] = X W^T for fp16 activations X [n, d_in], 1 <= n <= 64
         (n > 1 needs M of 2 or 4): what :func:`gemm_small_batch` computes on
         the row-major codes, bit for bit."""
         if x.dtype != torch.float16 or x.dim() != 2 or x.shape[1] != self.d_in or not x.is_cuda \

@@ -507,8 +507,22 @@ int aqlm_gemm_small_batch_tiled(const void* codes, const uint16_t* codebooks, co
     if (!aqlm::gemv_mfma_fits(&L, 1)) return AQLM_ERR_UNSUPPORTED;
     return status_of(aqlm::launch_gemv_mfma(&L, &x, &y, 1, s));
   }
-  if (!aqlm::gemm_nb_supported(L, (int32_t)n)) return AQLM_ERR_UNSUPPORTED;
-  return status_of(aqlm::launch_gemm_nb(L, (int32_t)n, x, y, s));
+  // up to 16 rows in one launch, up to 64 as launches of 16 (as the row-major
+  // product does)
+  if (n > kChunkedMax || !aqlm::gemm_nb_supported(L, (int32_t)(n < kSmallBatchMax ? n : kSmallBatchMax)))
+    return AQLM_ERR_UNSUPPORTED;
+  if (n % kSmallBatchMax == 1 && !aqlm::gemv_mfma_fits(&L, 1)) return AQLM_ERR_UNSUPPORTED;
+  for (int64_t t0 = 0; t0 < n; t0 += kSmallBatchMax) {
+    const int64_t nt = n - t0 < kSmallBatchMax ? n - t0 : kSmallBatchMax;
+    const uint16_t* xt = x + t0 * d_in;
+    uint16_t* yt = y + t0 * d_out;
+    // (a last chunk of one row is the matrix-vector product, as in the
+    // row-major path)
+    const hipError_t e = nt == 1 ? aqlm::launch_gemv_mfma(&L, &xt, &yt, 1, s)
+                                 : aqlm::launch_gemm_nb(L, (int32_t)nt, xt, yt, s);
+    if (e != hipSuccess) return AQLM_ERR_HIP;
+  }
+  return AQLM_OK;
 }
 
 int64_t aqlm_gemv_step_plan_bytes(int32_t levels) {

@@ -403,8 +403,9 @@ def test_tiled_grouped_validation_order(lib):
 
 def test_tiled_small_batch_validation(lib):
     """aqlm_gemm_small_batch_tiled: aqlm_gemm_small_batch's checks first, then
-    what the tiled product takes (1..16 rows; more than one row needs M of 2
-    or 4), all before anything is launched (fake pointers)."""
+    what the tiled product takes (1..64 rows; more than one row needs M of 2
+    or 4), all before anything is launched (fake pointers: every call here
+    must be refused)."""
     def call(codes=P, d_out=64, d_in=256, M=2, B=8, n=4, x=P, y=P):
         return lib.aqlm_gemm_small_batch_tiled(codes, P, P, d_out, d_in, M, B, 8, n, x, y, None)
     assert call(codes=None) == NULL
@@ -412,7 +413,8 @@ def test_tiled_small_batch_validation(lib):
     assert call(n=0) == SHAPE
     assert call(d_in=250) == SHAPE
     assert call(x=P + 8) == ALIGN
-    assert call(n=17) == UNSUP
+    assert call(n=65) == UNSUP
     assert call(M=1, n=2) == UNSUP
+    assert call(M=1, n=17) == UNSUP
     assert call(M=1, B=16) == UNSUP
     assert call(M=3) == UNSUP

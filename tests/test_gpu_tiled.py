@@ -174,9 +174,11 @@ def test_tiled_errors():
 
 
 # Small batch over tiled codes: (d_out, d_in, M, n) - ragged rows and
-# K-slices, the unaligned-pitch class, 7B shapes, 1..16 rows.
+# K-slices, the unaligned-pitch class, 7B shapes, 1..64 rows (chunks of 16,
+# a last chunk of one row).
 NB_CASES = [(37, 200, 2, 2), (1000, 4104, 2, 3), (100, 1032, 4, 16), (4096, 4096, 2, 4), (11008, 4096, 4, 16),
-            (4096, 11008, 2, 8), (256, 1024, 2, 1), (256, 1024, 1, 1)]
+            (4096, 11008, 2, 8), (256, 1024, 2, 1), (256, 1024, 1, 1), (300, 520, 2, 17), (1000, 1032, 4, 40),
+            (512, 4096, 2, 64)]
 
 
 @pytest.mark.parametrize("d_out,d_in,M,n", NB_CASES)
@@ -202,11 +204,11 @@ def test_gemm_small_batch_tiled_refusals():
     t = aq().TiledCodes(codes, cb, sc)
     with pytest.raises(RuntimeError):
         t.gemm_small_batch(x)  # M = 1 with two rows
-    lay = synth.layer(9991, 64, 256, 2, 8, n=17)
+    lay = synth.layer(9991, 64, 256, 2, 8, n=65)
     codes, cb, sc, x = to_device(lay)
     t = aq().TiledCodes(codes, cb, sc)
-    out = torch.full((17, 64), 5.0, dtype=torch.float16, device="cuda")
+    out = torch.full((65, 64), 5.0, dtype=torch.float16, device="cuda")
     with pytest.raises(RuntimeError):
-        t.gemm_small_batch(x, out=out)  # more than 16 rows
+        t.gemm_small_batch(x, out=out)  # more than 64 rows
     torch.cuda.synchronize()
     assert torch.all(out == 5.0)
