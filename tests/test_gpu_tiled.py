@@ -46,7 +46,8 @@ def tiled_layout(codes: np.ndarray) -> np.ndarray:
     return full.reshape(blocks, 16, ks, 64).transpose(0, 2, 1, 3).reshape(-1)
 
 
-TILE_SHAPES = [(16, 64, 2), (37, 200, 2), (1000, 4104, 2), (33, 1032, 1), (100, 520, 4), (8192, 8192, 2)]
+TILE_SHAPES = [(1, 8, 1), (16, 64, 2), (37, 200, 2), (1000, 4104, 2), (33, 1032, 1), (100, 520, 4),
+               (8192, 8192, 2)]
 
 
 @pytest.mark.parametrize("d_out,d_in,M", TILE_SHAPES)
@@ -64,6 +65,8 @@ def test_tile_codes_layout(d_out, d_in, M):
 # (shapes of one grouped launch, M): ragged rows and K-slices, the row-major
 # unaligned-pitch class, Llama-2 7B and 70B launches
 TILED_CASES = [
+    ([(1, 8)], 2),                       # one row, one group: a single, mostly padded tile
+    ([(1, 8), (5, 16)], 4),
     ([(37, 200)], 2),
     ([(1000, 4104), (64, 512), (3000, 2048), (17, 8)], 2),
     ([(100, 1032), (40, 520)], 2),
@@ -178,7 +181,7 @@ def test_tiled_errors():
 # a last chunk of one row).
 NB_CASES = [(37, 200, 2, 2), (1000, 4104, 2, 3), (100, 1032, 4, 16), (4096, 4096, 2, 4), (11008, 4096, 4, 16),
             (4096, 11008, 2, 8), (256, 1024, 2, 1), (256, 1024, 1, 1), (300, 520, 2, 17), (1000, 1032, 4, 40),
-            (512, 4096, 2, 64)]
+            (512, 4096, 2, 64), (1, 8, 2, 1), (1, 8, 4, 2), (3, 16, 2, 33)]
 
 
 @pytest.mark.parametrize("d_out,d_in,M,n", NB_CASES)
