@@ -922,13 +922,16 @@ hipError_t launch_ks(const GemvBatch& bt, size_t lds_bytes, hipStream_t s) {
 // spilling (1024 threads: 128 VGPRs per lane); M = 1 holds 16 x slices.
 constexpr int ks_rb_cap(int M) { return M == 1 ? 2 : 7; }
 
-// Ring depth in K-slices: up to about eight items in flight per wave, within
-// the register budget, and no more K-slices than a wave owns (extra slots
-// would only repeat its last one).  Paired row blocks need at least four
-// slots.
+// Ring depth in K-slices: up to eight single blocks in flight per wave, no
+// more K-slices than a wave owns (extra slots would only repeat its last
+// one), and for paired blocks two K-slices at most: with two or three items
+// requested ahead a deeper ring only moves K-slices out of the loop's
+// unconditional part (Llama-2-70B down, two blocks, seven K-slices per wave:
+// tiled step 4.858-4.869 ms with four, 4.837-4.852 with two, same box).
+// Paired row blocks need at least four slots.
 template <int M, int COPIES, int RB, bool VEC>
 hipError_t launch_ks_d(const GemvBatch& bt, int nks, size_t lds_bytes, hipStream_t s) {
-  constexpr int kDMax = RB >= 5 ? 1 : (RB >= 3 ? 2 : (RB == 2 ? 4 : 8));
+  constexpr int kDMax = RB >= 5 ? 1 : (RB >= 2 ? 2 : 8);
   constexpr int kDMin = (RB == 2 || RB == 3) ? 2 : 1;
   if constexpr (kDMax >= 8) {
     if (nks >= 8) return launch_ks<M, COPIES, RB, 8, VEC>(bt, lds_bytes, s);
@@ -999,9 +1002,9 @@ hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStrea
 // (M = 2, 8-bit codes, 16-byte code rows) body instantiations: (id, copies,
 // row blocks, ring depth)
 #define AQLM_STEP_VARIANTS(X)                                                                    \
-  X(0, 16, 1, 1) X(1, 16, 1, 2) X(2, 16, 1, 4) X(3, 16, 1, 8) X(4, 16, 2, 2) X(5, 16, 2, 4)       \
-  X(6, 16, 3, 2) X(7, 16, 4, 1) X(8, 16, 4, 2) X(9, 16, 5, 1) X(10, 16, 6, 1) X(11, 16, 7, 1)     \
-  X(12, 8, 1, 1) X(13, 8, 1, 2) X(14, 8, 1, 4) X(15, 8, 1, 8) X(16, 8, 2, 2) X(17, 8, 2, 4)
+  X(0, 16, 1, 1) X(1, 16, 1, 2) X(2, 16, 1, 4) X(3, 16, 1, 8) X(4, 16, 2, 2) X(6, 16, 3, 2)       \
+  X(7, 16, 4, 1) X(8, 16, 4, 2) X(9, 16, 5, 1) X(10, 16, 6, 1) X(11, 16, 7, 1) X(12, 8, 1, 1)      \
+  X(13, 8, 1, 2) X(14, 8, 1, 4) X(15, 8, 1, 8) X(16, 8, 2, 2)
 
 int step_variant(int M, int copies, int rb, int d, bool vec) {
   if (M != 2 || !vec) return -1;
@@ -1122,7 +1125,7 @@ bool gemv_mfma_fits(const Layer* Ls, int count) {
 // Ring depth k_gemv_ks runs for RB row blocks and nks K-slices per wave
 // (launch_ks_d's choice).
 int ks_ring_depth(int rb, int nks) {
-  const int dmax = rb >= 5 ? 1 : (rb >= 3 ? 2 : (rb == 2 ? 4 : 8));
+  const int dmax = rb >= 5 ? 1 : (rb >= 2 ? 2 : 8);
   const int dmin = (rb == 2 || rb == 3) ? 2 : 1;
   if (dmax >= 8 && nks >= 8) return 8;
   if (dmax >= 4 && nks >= 4) return 4;
