@@ -928,11 +928,13 @@ constexpr int ks_rb_cap(int M) { return M == 1 ? 2 : 7; }
 // requested ahead a deeper ring only moves K-slices out of the loop's
 // unconditional part (Llama-2-70B down, two blocks, seven K-slices per wave:
 // tiled step 4.858-4.869 ms with four, 4.837-4.852 with two, same box).
-// Paired row blocks need at least four slots.
+// Three blocks (three items ahead) fill a one-K-slice ring (q/k/v, two
+// K-slices per wave: 4.824-4.833 -> 4.803-4.814 ms); two blocks keep two
+// K-slices so that both items of the next pair have slots of their own.
 template <int M, int COPIES, int RB, bool VEC>
 hipError_t launch_ks_d(const GemvBatch& bt, int nks, size_t lds_bytes, hipStream_t s) {
-  constexpr int kDMax = RB >= 5 ? 1 : (RB >= 2 ? 2 : 8);
-  constexpr int kDMin = (RB == 2 || RB == 3) ? 2 : 1;
+  constexpr int kDMax = (RB >= 5 || RB == 3) ? 1 : (RB >= 2 ? 2 : 8);
+  constexpr int kDMin = RB == 2 ? 2 : 1;
   if constexpr (kDMax >= 8) {
     if (nks >= 8) return launch_ks<M, COPIES, RB, 8, VEC>(bt, lds_bytes, s);
   }
@@ -1002,7 +1004,7 @@ hipError_t launch_copies(const GemvBatch& bt, int pf, size_t lds_bytes, hipStrea
 // (M = 2, 8-bit codes, 16-byte code rows) body instantiations: (id, copies,
 // row blocks, ring depth)
 #define AQLM_STEP_VARIANTS(X)                                                                    \
-  X(0, 16, 1, 1) X(1, 16, 1, 2) X(2, 16, 1, 4) X(3, 16, 1, 8) X(4, 16, 2, 2) X(6, 16, 3, 2)       \
+  X(0, 16, 1, 1) X(1, 16, 1, 2) X(2, 16, 1, 4) X(3, 16, 1, 8) X(4, 16, 2, 2) X(6, 16, 3, 1)       \
   X(7, 16, 4, 1) X(8, 16, 4, 2) X(9, 16, 5, 1) X(10, 16, 6, 1) X(11, 16, 7, 1) X(12, 8, 1, 1)      \
   X(13, 8, 1, 2) X(14, 8, 1, 4) X(15, 8, 1, 8) X(16, 8, 2, 2)
 
@@ -1125,8 +1127,8 @@ bool gemv_mfma_fits(const Layer* Ls, int count) {
 // Ring depth k_gemv_ks runs for RB row blocks and nks K-slices per wave
 // (launch_ks_d's choice).
 int ks_ring_depth(int rb, int nks) {
-  const int dmax = rb >= 5 ? 1 : (rb >= 2 ? 2 : 8);
-  const int dmin = (rb == 2 || rb == 3) ? 2 : 1;
+  const int dmax = (rb >= 5 || rb == 3) ? 1 : (rb >= 2 ? 2 : 8);
+  const int dmin = rb == 2 ? 2 : 1;
   if (dmax >= 8 && nks >= 8) return 8;
   if (dmax >= 4 && nks >= 4) return 4;
   if (dmax >= 2 && (nks >= 2 || dmin == 2)) return 2;
